@@ -1,0 +1,192 @@
+"""Benchmark: one MoE layer's routing + Exact Quantile Balancing statistics.
+
+A step is the whole path over one batch already resident in HBM:
+  zero counters -> route_topk (+ fused coarse counts) -> select pass 1
+  -> fine counts (pass 2) -> select pass 2 (+ centred bias).
+
+    python bench.py [--gpus 1] [--steps 20] [--warmup 5] [--workload large256]
+
+Prints one JSON line.  ``value`` is tokens/s of the whole step; ``roofline``
+describes the dominant kernel (route + coarse pass), timed live with HIP
+events on the stream it runs on; ``cpu_baseline`` times the CPU oracle on a
+bounded slice of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0                     # MI355X HBM3E, vendor figure
+METRIC = "routing+EQB tokens/s per MoE layer; achieved HBM GB/s vs peak"
+SRC = os.path.join(ROOT, "paper_2609_28053_amd", "csrc", "eqb.hip")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "route_hist1_large256_traffic.txt")
+
+
+def route_bytes_per_token(E, K):
+    """Algorithmic bytes of route + coarse pass: read z row, write idx, score, tau."""
+    return 2 * E + 4 * K + 4 * K + 4
+
+
+def pass_bytes_per_token(E, K):
+    """Algorithmic bytes of the whole step: z twice, idx, score, tau written and read back."""
+    return 4 * E + 8 * K + 8
+
+
+def source_hash():
+    with open(SRC, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def read_traffic(T):
+    """Measured HBM bytes per launch of the route kernel from a committed
+    rocprofv3 counter summary, if it was taken on the current kernel source."""
+    if not os.path.exists(TRAFFIC_FILE):
+        return None
+    vals = {}
+    for line in open(TRAFFIC_FILE):
+        if "=" in line and not line.startswith("#"):
+            k, v = line.split("=", 1)
+            vals[k.strip()] = v.strip()
+    if vals.get("source_sha256_16") != source_hash() or int(vals.get("T", -1)) != T:
+        return None
+    try:
+        return float(vals["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def cpu_baseline(w, rows, threads=1):
+    import workloads as W
+    from oracle import eqb_oracle as O
+    sub = w.with_T(rows, 1)
+    z, b, off = W.generate(sub)
+    t0 = time.perf_counter()
+    O.run_layer(z, b, sub.K, off, threads=threads)
+    dt = time.perf_counter() - t0
+    return {"value": rows / dt, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "sample": f"first {rows} tokens of {w.name} (E={w.E}, K={w.K}, one partition), "
+                      f"full oracle layer (row sorts, margins, column sorts, counts) in "
+                      f"{dt:.1f} s on {threads} thread(s) of {os.cpu_count()} visible cores"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="large256")
+    ap.add_argument("--cpu-rows", type=int, default=262144,
+                    help="tokens in the CPU-oracle baseline slice (0 disables it)")
+    ap.add_argument("--stages", action="store_true", help="also print per-stage times to stderr")
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU: this build has no multi-GPU path "
+              "(the per-rank all-reduce of Algorithm 1 is reproduced as a sum of partition "
+              "histograms on one device). Run with --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import workloads as W
+    from paper_2609_28053_amd import eqb
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    w = W.CONFIGS[args.workload]
+    t0 = time.time()
+    z, b, off = W.generate(w)
+    print(f"[bench] generated {w.name} T={w.T} E={w.E} K={w.K} P={w.P} in {time.time() - t0:.1f}s",
+          file=sys.stderr, flush=True)
+    dev = torch.device("cuda:0")
+    zt = torch.from_numpy(z.view(np.int16)).to(dev)
+    bt = torch.from_numpy(b).to(dev)
+    del z
+    part_off = [int(x) for x in off]
+    r = eqb.eqb_rank(w.T, w.K, w.E)
+
+    stream = torch.cuda.Stream(device=dev)     # default priority
+    lay = eqb.Layer(w.T, w.E, w.K, w.P, device=dev)
+
+    def step(ev=None):
+        rec = (lambda i: ev[i].record(stream)) if ev else (lambda i: None)
+        rec(0)
+        lay._counts.zero_()
+        rec(1)
+        eqb.eqb_route_topk(zt, bt, w.K, lay.topk_idx, lay.topk_score, lay.tau, part_off,
+                           lay.load, lay.hist_hi, stream)
+        rec(2)
+        eqb.eqb_select_quantile(1, lay.hist_hi, r, lay.sel_hi, lay.rank_in_bin,
+                                hist_sum=lay.H, dev_status=lay.dev_status, stream=stream)
+        rec(3)
+        eqb.eqb_margin_hist_pass2(zt, lay.tau, lay.sel_hi, lay.hist_lo, part_off, stream)
+        rec(4)
+        eqb.eqb_select_quantile(2, lay.hist_lo, r, lay.sel_hi, lay.rank_in_bin, lay.sel_lo,
+                                lay.q_bf16, lay.b_next, hist_sum=lay.L, dev_status=lay.dev_status,
+                                stream=stream)
+        rec(5)
+
+    with torch.cuda.stream(stream):
+        for _ in range(args.warmup):
+            step()
+        # per-kernel durations come from HIP events recorded on the launch stream
+        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(6)] for _ in range(args.steps)]
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for i in range(args.steps):            # timed region: exactly `steps` steps
+            step(evs[i])
+        torch.cuda.synchronize()
+        elapsed = time.perf_counter() - t0
+    assert int(lay.dev_status.item()) == 0, "device reported a rank beyond the counts"
+
+    names = ["zero", "route_hist1", "select1", "margin_hist2", "select2"]
+    stage_ms = {n: float(np.mean([evs[i][j].elapsed_time(evs[i][j + 1]) for i in range(args.steps)]))
+                for j, n in enumerate(names)}
+    ms_per_step = elapsed * 1e3 / args.steps
+    tokens_per_s = w.T / (ms_per_step * 1e-3)
+    pass_gbs = pass_bytes_per_token(w.E, w.K) * w.T / (ms_per_step * 1e-3) / 1e9
+    route_bytes = route_bytes_per_token(w.E, w.K) * w.T
+    route_gbs = route_bytes / (stage_ms["route_hist1"] * 1e-3) / 1e9
+    traffic = read_traffic(w.T)
+
+    out = {
+        "metric": METRIC,
+        "value": tokens_per_s,
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": w.name, "T": w.T, "E": w.E, "K": w.K, "P": w.P,
+                   "logits": "bf16 N(0,1) + per-expert N(0,0.7) offset, 5% tokens +3 on one expert",
+                   "parallelism": "single GPU; P partitions summed on device"},
+        "pass_hbm_gbs": pass_gbs,
+        "pass_frac_of_peak": pass_gbs / HBM_PEAK_GBS,
+        "stage_ms": stage_ms,
+        "roofline": {"kernel": "route_hist1", "bound": "hbm", "achieved": route_gbs,
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": route_gbs / HBM_PEAK_GBS,
+                     "traffic": traffic, "algorithmic_bytes": route_bytes},
+    }
+    if args.cpu_rows > 0:
+        out["cpu_baseline"] = cpu_baseline(w, args.cpu_rows)
+    else:
+        out["cpu_baseline"] = None
+    if args.stages:
+        print(json.dumps(stage_ms), file=sys.stderr)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

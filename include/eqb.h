@@ -1,0 +1,144 @@
+/*
+ * eqb.h - C ABI of the MI355X (gfx950) library for one MoE layer's routing
+ * and Exact Quantile Balancing (EQB) statistics.
+ *
+ * Method: arXiv 2609.28053, "Exact Quantile Balancing and Load-Error Injection
+ * for Mixture-of-Experts".  Notation follows the paper:
+ *   z[T,E]   router logits (BF16), b[E] expert bias (binary32),
+ *   I_t      = Top-K(z_t + b)                          (Sec. 2, Eq. 1)
+ *   s_{t,e}  = sigmoid(z_{t,e}) for e in I_t, unbiased  (Sec. 2, Eq. 1)
+ *   f_e      = #{t : e in I_t}                          (Sec. 2)
+ *   tau_t    = (K+1)st largest entry of z_t + b         (Sec. 2, "Quantile Balancing")
+ *   margin   = tau_t - z_{t,e} as a BF16 value, key kappa = (h, l) (Appendix C, Algorithm 1)
+ *   r        = T*K/E, the rank of the balanced quantile  (Sec. 3)
+ *   H_{p,e,u}, L_{p,e,v}  coarse / fine counts of partition p (Algorithm 1, steps 1 and 4)
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ * Memory.  Every pointer is a DEVICE pointer except `part_off`, which is a
+ *   HOST array read during the call.  The caller allocates and owns every
+ *   buffer; the library allocates nothing and keeps no pointer after the call
+ *   returns.  Calls only enqueue work on `stream` (a hipStream_t, NULL = the
+ *   default stream) and never synchronise the host.
+ * Layouts.  Row-major.  z is [T,E] BF16 bit patterns (uint16), 16-byte
+ *   aligned.  topk_idx/topk_score are [T,K].  Count arrays are int32:
+ *   loads [P,E], coarse/fine histograms [P,E,256] (slab p = partition p).
+ * Partitions.  Tokens are split into P contiguous ranges
+ *   [part_off[p], part_off[p+1]), standing in for P data-parallel ranks.
+ *   part_off has P+1 entries, part_off[0] = 0, part_off[P] = T, non-decreasing
+ *   (empty partitions are allowed).  part_off = NULL means P = 1.  Summing the
+ *   slabs over p is the all-reduce of Algorithm 1, steps 2 and 5.
+ * Accumulation.  Histogram and load outputs are ACCUMULATED (+=): zero them
+ *   before the first call of a layer.
+ * Numerics.  z + b and tau - z are single binary32 operations rounded to
+ *   nearest even, with subnormals kept; a margin is rounded once to BF16
+ *   (nearest, ties to even).  kappa(bits) = bits ^ (sign ? 0xFFFF : 0x8000),
+ *   which orders BF16 values as IEEE totalOrder (-0 < +0).  Top-K ties go to
+ *   the lower expert index (-0 and +0 are equal there); I_t is written in rank
+ *   order (score descending, then index ascending).  Inputs must be finite.
+ * Supported shapes.  E in {8, 16, 32, 64, 128, 256}; 1 <= K < E;
+ *   0 <= T < 2^31; 1 <= P <= EQB_MAX_PARTITIONS.
+ * Errors.  Every argument check runs before anything is enqueued, so a call
+ *   that returns an error has left the stream untouched.  T = 0 returns
+ *   EQB_OK and enqueues nothing.
+ */
+#ifndef EQB_H
+#define EQB_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t eqb_status;
+
+#define EQB_OK               0
+#define EQB_ERR_INVALID_ARG  1   /* null pointer, bad K/T/P, bad partition table */
+#define EQB_ERR_UNSUPPORTED  2   /* E outside the supported set, misaligned z */
+#define EQB_ERR_RANK         3   /* r < 1 or r > number of counted margins */
+#define EQB_ERR_HIP          4   /* the HIP runtime reported a launch error */
+
+#define EQB_NBINS            256
+#define EQB_MAX_PARTITIONS   256
+
+/* Device status word written by eqb_select_quantile. */
+#define EQB_DEV_OK                 0
+#define EQB_DEV_RANK_EXCEEDS_COUNT 1   /* an expert holds fewer than r (or rho) counts */
+
+/*
+ * Routing (Sec. 2, Eq. 1 and "Quantile Balancing"), optionally fused with
+ * the coarse pass of Algorithm 1 (step 1).
+ *   z [T,E] bf16 bits, b [E] binary32                     (in)
+ *   topk_idx [T,K] int32, topk_score [T,K] binary32,
+ *   tau [T] binary32                                      (out)
+ *   load [P,E] int32 (nullable)                           (+= f_{p,e})
+ *   hist_hi [P,E,256] int32 (nullable)                    (+= H_{p,e,u}, u = h of the margin key)
+ * tau_t carries the bit pattern of the entry at rank K (0-based).
+ * Returns EQB_ERR_INVALID_ARG, EQB_ERR_UNSUPPORTED or EQB_ERR_HIP on failure.
+ */
+eqb_status eqb_route_topk(const uint16_t* z, const float* b, int64_t T, int32_t E, int32_t K,
+                          int32_t* topk_idx, float* topk_score, float* tau,
+                          const int64_t* part_off, int32_t P,
+                          int32_t* load, int32_t* hist_hi, void* stream);
+
+/*
+ * Coarse pass alone (Algorithm 1, step 1): hist_hi[p,e,u] += #{t in p : h_{t,e} = u},
+ * where (h, l) = kappa(bf16(tau_t - z_{t,e})).
+ *   z [T,E] bf16 bits, tau [T] binary32 (in); hist_hi [P,E,256] int32 (+=).
+ */
+eqb_status eqb_margin_hist_pass1(const uint16_t* z, const float* tau, int64_t T, int32_t E,
+                                 const int64_t* part_off, int32_t P, int32_t* hist_hi,
+                                 void* stream);
+
+/*
+ * Selection (Algorithm 1, steps 2-3 for pass = 1; steps 5-6 for pass = 2).
+ * Both passes first sum the P slabs of `hist` (the all-reduce, steps 2 and 5).
+ * pass = 1: hist = H_p [P,E,256].  Writes sel_hi[e] = u_e = min{u : sum_{j<=u} H[e,j] >= r}
+ *   and rank_in_bin[e] = rho_e = r - sum_{j<u_e} H[e,j].
+ * pass = 2: hist = L_p [P,E,256], reads sel_hi and rank_in_bin.  Writes
+ *   sel_lo[e] = v_e = min{v : sum_{j<=v} L[e,j] >= rho_e}, q_bf16[e] = kappa^-1(u_e, v_e)
+ *   (the exact r-th smallest BF16 margin, b_hat_e) and, if b_next != NULL,
+ *   the centred bias b_next[e] = b_hat_e - mean(b_hat) (Eq. 2): a binary64 sum in
+ *   ascending e, divided by E, subtracted in binary64 and rounded once to binary32.
+ *   r is the rank over the whole batch (all partitions), see eqb_rank.
+ *   hist_sum [E,256] int32 (nullable): receives the summed counts.
+ *   dev_status (nullable, int32): set to EQB_DEV_RANK_EXCEEDS_COUNT when some
+ *   expert holds fewer than r (pass 1) or rho_e (pass 2) counts; it is never
+ *   cleared by the library.  The affected sel_hi/sel_lo entries are -1 and
+ *   q_bf16 is a NaN pattern.
+ * Returns EQB_ERR_RANK if r < 1; other errors as above.
+ */
+eqb_status eqb_select_quantile(int32_t pass, const int32_t* hist, int32_t P, int32_t E, int64_t r,
+                               int32_t* sel_hi, int64_t* rank_in_bin,
+                               int32_t* sel_lo, uint16_t* q_bf16, float* b_next,
+                               int32_t* hist_sum, int32_t* dev_status, void* stream);
+
+/*
+ * Fine pass (Algorithm 1, step 4): rescans z and tau and, for margins whose
+ * high byte equals sel_hi[e] = u_e, hist_lo[p,e,v] += #{t in p : h_{t,e} = u_e, l_{t,e} = v}.
+ *   z [T,E] bf16 bits, tau [T], sel_hi [E] int32 (in); hist_lo [P,E,256] int32 (+=).
+ */
+eqb_status eqb_margin_hist_pass2(const uint16_t* z, const float* tau, int64_t T, int32_t E,
+                                 const int32_t* sel_hi, const int64_t* part_off, int32_t P,
+                                 int32_t* hist_lo, void* stream);
+
+/*
+ * Expert loads (Sec. 2): load[p,e] += #{t in p : e in I_t} from topk_idx [T,K].
+ * Entries outside [0, E) are not counted.
+ */
+eqb_status eqb_expert_load(const int32_t* topk_idx, int64_t T, int32_t K, int32_t E,
+                           const int64_t* part_off, int32_t P, int32_t* load, void* stream);
+
+/* Host helper: r = ceil(T*K/E) (Sec. 3; the paper assumes T*K/E is an
+ * integer), or -1 for invalid arguments.  Host only, no HIP call. */
+int64_t eqb_rank(int64_t T_total, int32_t K, int32_t E);
+
+/* Host helper: a static string naming a status code. */
+const char* eqb_status_string(eqb_status status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* EQB_H */

@@ -1,0 +1,232 @@
+"""ctypes binding of libeqb.so: argument marshalling only.
+
+Every function takes torch tensors that live on the GPU (except ``part_off``,
+a host sequence of P+1 token offsets) and passes their device pointers and the
+current HIP stream to the C ABI of the same name.  All computation happens in
+the library's kernels; torch only provides device memory and streams.  A
+missing or unloadable library raises ImportError: there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence
+
+import numpy as np
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.environ.get("EQB_LIB", os.path.join(_HERE, "libeqb.so"))
+
+EQB_OK = 0
+EQB_ERR_INVALID_ARG = 1
+EQB_ERR_UNSUPPORTED = 2
+EQB_ERR_RANK = 3
+EQB_ERR_HIP = 4
+EQB_NBINS = 256
+EQB_MAX_PARTITIONS = 256
+EQB_DEV_RANK_EXCEEDS_COUNT = 1
+
+EXPORTS = (
+    "eqb_route_topk",
+    "eqb_margin_hist_pass1",
+    "eqb_select_quantile",
+    "eqb_margin_hist_pass2",
+    "eqb_expert_load",
+    "eqb_rank",
+    "eqb_status_string",
+)
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"libeqb.so not built at {LIB_PATH}; run paper_2609_28053_amd/build.py")
+    try:
+        lib = ctypes.CDLL(LIB_PATH)
+    except OSError as exc:  # pragma: no cover - depends on the ROCm install
+        raise ImportError(f"cannot load {LIB_PATH}: {exc}") from exc
+    P = ctypes.c_void_p
+    i32, i64 = ctypes.c_int32, ctypes.c_int64
+    sig = {
+        "eqb_route_topk": [P, P, i64, i32, i32, P, P, P, P, i32, P, P, P],
+        "eqb_margin_hist_pass1": [P, P, i64, i32, P, i32, P, P],
+        "eqb_select_quantile": [i32, P, i32, i32, i64, P, P, P, P, P, P, P, P],
+        "eqb_margin_hist_pass2": [P, P, i64, i32, P, P, i32, P, P],
+        "eqb_expert_load": [P, i64, i32, i32, P, i32, P, P],
+        "eqb_rank": [i64, i32, i32],
+        "eqb_status_string": [i32],
+    }
+    for name, args in sig.items():
+        fn = getattr(lib, name)
+        fn.argtypes = args
+        fn.restype = i32
+    lib.eqb_rank.restype = i64
+    lib.eqb_status_string.restype = ctypes.c_char_p
+    return lib
+
+
+lib = _load()
+
+
+class EqbError(RuntimeError):
+    def __init__(self, name: str, status: int):
+        self.status = status
+        super().__init__(f"{name} returned {lib.eqb_status_string(status).decode()} ({status})")
+
+
+def _check(name: str, status: int) -> None:
+    if status != EQB_OK:
+        raise EqbError(name, status)
+
+
+def _ptr(t: Optional[torch.Tensor], dtype=None, numel=None, name="tensor"):
+    if t is None:
+        return None
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch tensor")
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a GPU tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if dtype is not None and t.dtype not in (dtype if isinstance(dtype, tuple) else (dtype,)):
+        raise TypeError(f"{name} has dtype {t.dtype}, expected {dtype}")
+    if numel is not None and t.numel() != numel:
+        raise ValueError(f"{name} has {t.numel()} elements, expected {numel}")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream) -> ctypes.c_void_p:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream))
+
+
+def _offsets(part_off: Optional[Sequence[int]], T: int):
+    if part_off is None:
+        return None, 1, None
+    arr = np.ascontiguousarray(np.asarray(part_off, dtype=np.int64))
+    P = arr.size - 1
+    return arr.ctypes.data_as(ctypes.c_void_p), P, arr     # keep arr alive
+
+
+_Z = (torch.int16, torch.uint16) if hasattr(torch, "uint16") else (torch.int16,)
+
+
+def eqb_route_topk(z, b, K, topk_idx, topk_score, tau, part_off=None, load=None, hist_hi=None,
+                   stream=None):
+    T, E = z.shape
+    po, P, keep = _offsets(part_off, T)
+    _check("eqb_route_topk", lib.eqb_route_topk(
+        _ptr(z, _Z, name="z"), _ptr(b, torch.float32, E, "b"), T, E, K,
+        _ptr(topk_idx, torch.int32, T * K, "topk_idx"), _ptr(topk_score, torch.float32, T * K, "topk_score"),
+        _ptr(tau, torch.float32, T, "tau"), po, P,
+        _ptr(load, torch.int32, P * E, "load"), _ptr(hist_hi, torch.int32, P * E * EQB_NBINS, "hist_hi"),
+        _stream(stream)))
+    del keep
+
+
+def eqb_margin_hist_pass1(z, tau, hist_hi, part_off=None, stream=None):
+    T, E = z.shape
+    po, P, keep = _offsets(part_off, T)
+    _check("eqb_margin_hist_pass1", lib.eqb_margin_hist_pass1(
+        _ptr(z, _Z, name="z"), _ptr(tau, torch.float32, T, "tau"), T, E, po, P,
+        _ptr(hist_hi, torch.int32, P * E * EQB_NBINS, "hist_hi"), _stream(stream)))
+    del keep
+
+
+def eqb_select_quantile(pass_, hist, r, sel_hi, rank_in_bin, sel_lo=None, q_bf16=None, b_next=None,
+                        hist_sum=None, dev_status=None, stream=None):
+    P, E, nb = hist.shape
+    assert nb == EQB_NBINS
+    _check("eqb_select_quantile", lib.eqb_select_quantile(
+        pass_, _ptr(hist, torch.int32, name="hist"), P, E, r,
+        _ptr(sel_hi, torch.int32, E, "sel_hi"), _ptr(rank_in_bin, torch.int64, E, "rank_in_bin"),
+        _ptr(sel_lo, torch.int32, E, "sel_lo"), _ptr(q_bf16, _Z, E, "q_bf16"),
+        _ptr(b_next, torch.float32, E, "b_next"), _ptr(hist_sum, torch.int32, E * EQB_NBINS, "hist_sum"),
+        _ptr(dev_status, torch.int32, 1, "dev_status"), _stream(stream)))
+
+
+def eqb_margin_hist_pass2(z, tau, sel_hi, hist_lo, part_off=None, stream=None):
+    T, E = z.shape
+    po, P, keep = _offsets(part_off, T)
+    _check("eqb_margin_hist_pass2", lib.eqb_margin_hist_pass2(
+        _ptr(z, _Z, name="z"), _ptr(tau, torch.float32, T, "tau"), T, E,
+        _ptr(sel_hi, torch.int32, E, "sel_hi"), po, P,
+        _ptr(hist_lo, torch.int32, P * E * EQB_NBINS, "hist_lo"), _stream(stream)))
+    del keep
+
+
+def eqb_expert_load(topk_idx, E, load, part_off=None, stream=None):
+    T, K = topk_idx.shape
+    po, P, keep = _offsets(part_off, T)
+    _check("eqb_expert_load", lib.eqb_expert_load(
+        _ptr(topk_idx, torch.int32, T * K, "topk_idx"), T, K, E, po, P,
+        _ptr(load, torch.int32, P * E, "load"), _stream(stream)))
+    del keep
+
+
+def eqb_rank(T_total: int, K: int, E: int) -> int:
+    return int(lib.eqb_rank(T_total, K, E))
+
+
+class Layer:
+    """Device buffers for one layer's routing + EQB statistics, reused across calls."""
+
+    def __init__(self, T: int, E: int, K: int, P: int = 1, device="cuda"):
+        self.T, self.E, self.K, self.P = T, E, K, P
+        dev = torch.device(device)
+        i32 = dict(dtype=torch.int32, device=dev)
+        self.topk_idx = torch.empty((T, K), **i32)
+        self.topk_score = torch.empty((T, K), dtype=torch.float32, device=dev)
+        self.tau = torch.empty(T, dtype=torch.float32, device=dev)
+        # counters that are zeroed before every pass, kept in one buffer so a
+        # single fill clears them all
+        n_load, n_hist = P * E, P * E * EQB_NBINS
+        self._counts = torch.empty(n_load + 2 * n_hist + 1, **i32)
+        self.load = self._counts[:n_load].view(P, E)
+        self.hist_hi = self._counts[n_load:n_load + n_hist].view(P, E, EQB_NBINS)
+        self.hist_lo = self._counts[n_load + n_hist:n_load + 2 * n_hist].view(P, E, EQB_NBINS)
+        self.dev_status = self._counts[-1:]
+        self.H = torch.empty((E, EQB_NBINS), **i32)
+        self.L = torch.empty((E, EQB_NBINS), **i32)
+        self.sel_hi = torch.empty(E, **i32)
+        self.sel_lo = torch.empty(E, **i32)
+        self.rank_in_bin = torch.empty(E, dtype=torch.int64, device=dev)
+        self.q_bf16 = torch.empty(E, dtype=torch.int16, device=dev)
+        self.b_next = torch.empty(E, dtype=torch.float32, device=dev)
+
+    def run(self, z, b, part_off=None, fused=True, stream=None):
+        """One layer: route (+ coarse counts), select 1, fine counts, select 2."""
+        r = eqb_rank(self.T, self.K, self.E)
+        self._counts.zero_()
+        if fused:
+            eqb_route_topk(z, b, self.K, self.topk_idx, self.topk_score, self.tau, part_off,
+                           self.load, self.hist_hi, stream)
+        else:
+            eqb_route_topk(z, b, self.K, self.topk_idx, self.topk_score, self.tau, part_off,
+                           None, None, stream)
+            eqb_expert_load(self.topk_idx, self.E, self.load, part_off, stream)
+            eqb_margin_hist_pass1(z, self.tau, self.hist_hi, part_off, stream)
+        eqb_select_quantile(1, self.hist_hi, r, self.sel_hi, self.rank_in_bin,
+                            hist_sum=self.H, dev_status=self.dev_status, stream=stream)
+        eqb_margin_hist_pass2(z, self.tau, self.sel_hi, self.hist_lo, part_off, stream)
+        eqb_select_quantile(2, self.hist_lo, r, self.sel_hi, self.rank_in_bin, self.sel_lo,
+                            self.q_bf16, self.b_next, hist_sum=self.L, dev_status=self.dev_status,
+                            stream=stream)
+        return self
+
+    def results(self) -> dict:
+        """Copy every output to host numpy arrays (synchronises)."""
+        torch.cuda.synchronize()
+        g = lambda t: t.cpu().numpy()
+        return dict(idx=g(self.topk_idx), score=g(self.topk_score), tau=g(self.tau), load=g(self.load),
+                    H_p=g(self.hist_hi), H=g(self.H), u=g(self.sel_hi), rho=g(self.rank_in_bin),
+                    L_p=g(self.hist_lo), L=g(self.L), v=g(self.sel_lo),
+                    bhat=g(self.q_bf16).view(np.uint16), b_next=g(self.b_next),
+                    dev_status=int(self.dev_status.item()), r=eqb_rank(self.T, self.K, self.E))
+
+
+def run_layer(z: torch.Tensor, b: torch.Tensor, K: int, part_off=None, fused=True, stream=None) -> Layer:
+    T, E = z.shape
+    P = 1 if part_off is None else len(part_off) - 1
+    return Layer(T, E, K, P, device=z.device).run(z, b, part_off, fused, stream)

@@ -1,0 +1,134 @@
+"""The C ABI without a GPU: the library loads, exports every declared entry
+point, and rejects bad arguments before it touches the HIP runtime."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "eqb.h")
+LIB = os.path.join(ROOT, "paper_2609_28053_amd", "libeqb.so")
+
+OK, INVALID, UNSUPPORTED, RANK = 0, 1, 2, 3
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(eqb_[a-z0-9_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(LIB):
+        pytest.fail("libeqb.so is not built (run paper_2609_28053_amd/build.py)")
+    lib = ctypes.CDLL(LIB)
+    V, i32, i64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
+    lib.eqb_route_topk.argtypes = [V, V, i64, i32, i32, V, V, V, V, i32, V, V, V]
+    lib.eqb_margin_hist_pass1.argtypes = [V, V, i64, i32, V, i32, V, V]
+    lib.eqb_margin_hist_pass2.argtypes = [V, V, i64, i32, V, V, i32, V, V]
+    lib.eqb_select_quantile.argtypes = [i32, V, i32, i32, i64, V, V, V, V, V, V, V, V]
+    lib.eqb_expert_load.argtypes = [V, i64, i32, i32, V, i32, V, V]
+    lib.eqb_rank.argtypes = [i64, i32, i32]
+    lib.eqb_rank.restype = i64
+    lib.eqb_status_string.argtypes = [i32]
+    lib.eqb_status_string.restype = ctypes.c_char_p
+    return lib
+
+
+def test_header_declares_the_five_calls():
+    names = declared_functions()
+    for n in ("eqb_route_topk", "eqb_margin_hist_pass1", "eqb_margin_hist_pass2",
+              "eqb_select_quantile", "eqb_expert_load"):
+        assert n in names
+
+
+def test_every_declared_symbol_is_exported(lib):
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+
+
+def test_binding_exports_match_header():
+    src = open(os.path.join(ROOT, "paper_2609_28053_amd", "eqb.py")).read()
+    for name in declared_functions():
+        assert f'"{name}"' in src
+
+
+FAKE = ctypes.c_void_p(0x10000)     # never dereferenced: every call below fails its checks first
+
+
+def offs(*v):
+    arr = (ctypes.c_int64 * len(v))(*v)
+    return ctypes.cast(arr, ctypes.c_void_p), arr
+
+
+def route(lib, T=64, E=8, K=2, z=FAKE, po=None, P=1):
+    return lib.eqb_route_topk(z, FAKE, T, E, K, FAKE, FAKE, FAKE, po, P, None, None, None)
+
+
+def test_route_argument_checks(lib):
+    assert route(lib, K=0) == INVALID
+    assert route(lib, K=8) == INVALID            # K >= E
+    assert route(lib, T=-1) == INVALID
+    assert route(lib, E=12, K=2) == UNSUPPORTED
+    assert route(lib, E=512, K=2) == UNSUPPORTED
+    assert route(lib, z=ctypes.c_void_p(0x10002)) == UNSUPPORTED   # z not 16-byte aligned
+    assert lib.eqb_route_topk(None, FAKE, 64, 8, 2, FAKE, FAKE, FAKE, None, 1, None, None, None) == INVALID
+    assert lib.eqb_route_topk(FAKE, FAKE, 64, 8, 2, None, FAKE, FAKE, None, 1, None, None, None) == INVALID
+    assert route(lib, T=0) == OK                 # empty batch: nothing to do
+    assert lib.eqb_route_topk(None, None, 0, 8, 2, None, None, None, None, 1, None, None, None) == OK
+
+
+def test_partition_table_checks(lib):
+    po, keep = offs(0, 10, 5, 64)                 # decreasing
+    assert route(lib, po=po, P=3) == INVALID
+    po, keep = offs(0, 10, 63)                    # does not end at T
+    assert route(lib, po=po, P=2) == INVALID
+    po, keep = offs(1, 10, 64)                    # does not start at 0
+    assert route(lib, po=po, P=2) == INVALID
+    assert route(lib, po=None, P=2) == INVALID    # NULL table means exactly one partition
+    po, keep = offs(0, 64)
+    assert route(lib, po=po, P=0) == INVALID
+    big = [0] * 258
+    big[-1] = 64
+    po, keep = offs(*big)
+    assert route(lib, po=po, P=257) == INVALID    # beyond EQB_MAX_PARTITIONS
+    po, keep = offs(0, 0, 0)
+    assert route(lib, T=0, po=po, P=2) == OK      # all partitions empty
+
+
+def test_pass_and_load_checks(lib):
+    f = lib.eqb_margin_hist_pass1
+    assert f(FAKE, FAKE, 10, 12, None, 1, FAKE, None) == UNSUPPORTED
+    assert f(FAKE, None, 10, 8, None, 1, FAKE, None) == INVALID
+    assert f(FAKE, FAKE, 10, 8, None, 1, None, None) == INVALID
+    assert f(FAKE, FAKE, 0, 8, None, 1, FAKE, None) == OK
+    g = lib.eqb_margin_hist_pass2
+    assert g(FAKE, FAKE, 10, 8, None, None, 1, FAKE, None) == INVALID     # no sel_hi
+    assert g(ctypes.c_void_p(0x10008), FAKE, 10, 8, FAKE, None, 1, FAKE, None) == UNSUPPORTED
+    h = lib.eqb_expert_load
+    assert h(FAKE, 10, 0, 8, None, 1, FAKE, None) == INVALID
+    assert h(FAKE, 10, 2, 8, None, 1, None, None) == INVALID
+    assert h(FAKE, 10, 2, 7, None, 1, FAKE, None) == UNSUPPORTED
+
+
+def test_select_checks(lib):
+    s = lib.eqb_select_quantile
+    assert s(3, FAKE, 1, 8, 10, FAKE, FAKE, None, None, None, None, None, None) == INVALID
+    assert s(1, FAKE, 0, 8, 10, FAKE, FAKE, None, None, None, None, None, None) == INVALID
+    assert s(1, FAKE, 1, 9, 10, FAKE, FAKE, None, None, None, None, None, None) == UNSUPPORTED
+    assert s(1, FAKE, 1, 8, 0, FAKE, FAKE, None, None, None, None, None, None) == RANK
+    assert s(1, None, 1, 8, 5, FAKE, FAKE, None, None, None, None, None, None) == INVALID
+    assert s(2, FAKE, 1, 8, 5, FAKE, FAKE, None, FAKE, None, None, None, None) == INVALID  # no sel_lo
+
+
+def test_rank_and_status_strings(lib):
+    assert lib.eqb_rank(4096, 2, 8) == 1024
+    assert lib.eqb_rank(4194304, 8, 256) == 131072
+    assert lib.eqb_rank(10, 3, 8) == 4
+    assert lib.eqb_rank(10, 8, 8) == -1
+    assert lib.eqb_rank(-1, 2, 8) == -1
+    assert lib.eqb_status_string(0) == b"EQB_OK"
+    assert lib.eqb_status_string(3) == b"EQB_ERR_RANK"
+    assert lib.eqb_status_string(99) == b"EQB_ERR_UNKNOWN"

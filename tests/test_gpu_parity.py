@@ -1,0 +1,240 @@
+"""GPU parity: the HIP path through the C ABI against the CPU oracle.
+
+Integer outputs (Top-K indices, loads, coarse/fine counts, u, rho, v), tau,
+the BF16 quantile and the centred bias are compared bit for bit; the sigmoid
+scores within 1e-6 relative.  Inputs come from the seeded workload
+generators; nothing the GPU computes is fed to the oracle.
+"""
+import functools
+import os
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import workloads as W
+from oracle import eqb_oracle as O
+
+pytestmark = pytest.mark.gpu
+
+SCORE_RTOL = 1e-6
+
+
+def _threads():
+    try:
+        n = len(os.sched_getaffinity(0))
+    except AttributeError:  # pragma: no cover
+        n = os.cpu_count() or 1
+    return max(1, min(16, n))
+
+
+@pytest.fixture(scope="module")
+def eqb():
+    assert torch.cuda.is_available(), "GPU tests need a visible GPU"
+    from paper_2609_28053_amd import eqb as binding
+    return binding
+
+
+def say(msg):
+    print(f"[gpu-parity] {msg}", flush=True)
+    sys.stdout.flush()
+
+
+def gpu_layer(eqb, z, b, K, part_off, fused=True):
+    zt = torch.from_numpy(np.ascontiguousarray(z).view(np.int16)).cuda()
+    bt = torch.from_numpy(np.ascontiguousarray(b, np.float32)).cuda()
+    off = None if part_off is None else [int(x) for x in part_off]
+    lay = eqb.run_layer(zt, bt, K, off, fused=fused)
+    return lay.results()
+
+
+def assert_parity(got, want, K, check_parts=True):
+    assert got["dev_status"] == 0
+    np.testing.assert_array_equal(got["idx"], want["idx"])
+    np.testing.assert_array_equal(got["tau"].view(np.uint32), want["tau"].view(np.uint32))
+    ws = want["score"].astype(np.float64)
+    err = np.abs(got["score"].astype(np.float64) - ws)
+    assert np.all(err <= SCORE_RTOL * np.abs(ws)), float(np.max(err / np.abs(ws)))
+    if check_parts:
+        np.testing.assert_array_equal(got["load"], want["load"])
+        np.testing.assert_array_equal(got["H_p"], want["H_p"])
+        np.testing.assert_array_equal(got["L_p"], want["L_p"])
+    np.testing.assert_array_equal(got["load"].sum(0), want["load"].sum(0))
+    np.testing.assert_array_equal(got["H"], want["H"])
+    np.testing.assert_array_equal(got["L"], want["L"])
+    assert got["r"] == want["r"]
+    np.testing.assert_array_equal(got["u"], want["u"])
+    np.testing.assert_array_equal(got["rho"], want["rho"])
+    np.testing.assert_array_equal(got["v"], want["v"])
+    np.testing.assert_array_equal(got["bhat"], want["bhat"])
+    np.testing.assert_array_equal(got["b_next"].view(np.uint32), want["b_next"].view(np.uint32))
+
+
+@functools.lru_cache(maxsize=4)
+def workload(name, T=None, P=None):
+    w = W.CONFIGS[name] if T is None else W.CONFIGS[name].with_T(T, P)
+    z, b, off = W.generate(w)
+    return w, z, b, off
+
+
+@functools.lru_cache(maxsize=2)
+def oracle_for(name, T=None, P=None):
+    w, z, b, off = workload(name, T, P)
+    return O.run_layer(z, b, w.K, off, threads=_threads())
+
+
+# ------------------------------------------------- multi-tile, ragged -----
+SMALL = [("tiny", 4096 + 517, 3), ("skew64", 20011, 4), ("split128", 9973, 8),
+         ("tie64", 16411, 2), ("large256", 7001, 16)]
+
+
+@pytest.mark.parametrize("name,T,P", SMALL, ids=[s[0] for s in SMALL])
+def test_parity_small(eqb, name, T, P):
+    w, z, b, off = workload(name, T, P)
+    say(f"small {name} T={T} E={w.E} K={w.K} P={P}")
+    want = oracle_for(name, T, P)
+    assert_parity(gpu_layer(eqb, z, b, w.K, off, fused=True), want, w.K)
+    assert_parity(gpu_layer(eqb, z, b, w.K, off, fused=False), want, w.K)
+
+
+# ---------------------------------------------------------- full sizes ----
+@pytest.mark.parametrize("name", W.CONFIG_ORDER)
+def test_parity_full_size(eqb, name):
+    w, z, b, off = workload(name)
+    say(f"full {name} T={w.T} E={w.E} K={w.K} P={w.P} oracle threads={_threads()}")
+    want = oracle_for(name)
+    say(f"full {name}: oracle done, running GPU")
+    got = gpu_layer(eqb, z, b, w.K, off)
+    assert_parity(got, want, w.K)
+    # partition invariance: one partition gives the same statistics
+    one = gpu_layer(eqb, z, b, w.K, None)
+    for k in ("H", "L", "u", "v", "rho", "bhat", "b_next", "idx", "tau"):
+        np.testing.assert_array_equal(one[k], got[k])
+    np.testing.assert_array_equal(one["load"][0], got["load"].sum(0))
+
+
+# ------------------------------------------------------------ edge cases --
+@pytest.mark.parametrize("E", [8, 16, 32, 64, 128, 256])
+def test_every_E_and_K_extremes(eqb, E):
+    rng = np.random.default_rng(E)
+    for T in (1, 37, 2 * 1024 + 5):
+        z = O.f32_to_bf16_rne((rng.standard_normal((T, E)) * 2).astype(np.float32))
+        b = (rng.standard_normal(E) * 0.3).astype(np.float32)
+        for K in sorted({1, E // 2, E - 1}):
+            say(f"edge E={E} T={T} K={K}")
+            off = np.array([0, T // 3, T // 3, T], np.int64)
+            assert_parity(gpu_layer(eqb, z, b, K, off), O.run_layer(z, b, K, off), K)
+
+
+def test_all_ties_constant_logits(eqb):
+    for E, K in ((8, 2), (64, 6), (256, 8)):
+        T = 3000
+        z = np.full((T, E), 0x3F00, np.uint16)                 # every logit 0.5
+        b = np.zeros(E, np.float32)
+        say(f"constant logits E={E}")
+        want = O.run_layer(z, b, K)
+        got = gpu_layer(eqb, z, b, K, None)
+        assert_parity(got, want, K)
+        assert np.all(got["idx"] == np.arange(K))               # lower index wins every tie
+
+
+def test_signed_zeros_and_subnormals(eqb):
+    rng = np.random.default_rng(3)
+    T, E, K = 5000, 64, 4
+    pick = rng.integers(0, 6, size=(T, E))
+    table = np.array([0x0000, 0x8000, 0x0001, 0x8001, 0x007F, 0x3F80], np.uint16)
+    z = table[pick]
+    b = np.where(rng.random(E) < 0.5, np.float32(-0.0), np.float32(0.0)).astype(np.float32)
+    b[:4] = np.array([1e-40, -1e-40, 0.0, -0.0], np.float32)    # binary32 subnormals
+    say("signed zeros and subnormals")
+    assert_parity(gpu_layer(eqb, z, b, K, [0, 100, T]), O.run_layer(z, b, K, [0, 100, T]), K)
+
+
+def test_wide_range_logits(eqb):
+    rng = np.random.default_rng(4)
+    T, E, K = 4000, 128, 8
+    x = rng.standard_normal((T, E)) * np.exp(rng.uniform(-30, 30, size=(T, E)))
+    z = O.f32_to_bf16_rne(np.clip(x, -1e30, 1e30).astype(np.float32))
+    b = (rng.standard_normal(E) * 1e-3).astype(np.float32)
+    say("wide-range logits")
+    assert_parity(gpu_layer(eqb, z, b, K, None), O.run_layer(z, b, K), K)
+
+
+def test_empty_and_single_token_partitions(eqb):
+    w, z, b, _ = workload("skew64", 3001, 4)
+    off = np.array([0, 0, 1, 1, 1500, 1501, 3001, 3001], np.int64)
+    say("empty partitions")
+    assert_parity(gpu_layer(eqb, z, b, w.K, off), O.run_layer(z, b, w.K, off), w.K)
+
+
+def test_deterministic_repeat(eqb):
+    w, z, b, off = workload("large256", 20000, 16)
+    say("determinism")
+    a = gpu_layer(eqb, z, b, w.K, off)
+    c = gpu_layer(eqb, z, b, w.K, off)
+    for k in a:
+        np.testing.assert_array_equal(np.asarray(a[k]), np.asarray(c[k]))
+
+
+def test_standalone_calls_match_fused(eqb):
+    """eqb_margin_hist_pass1 and eqb_expert_load against the fused sweep."""
+    w, z, b, off = workload("split128", 12345, 8)
+    say("standalone pass 1 and load")
+    zt = torch.from_numpy(z.view(np.int16)).cuda()
+    bt = torch.from_numpy(b).cuda()
+    offl = [int(x) for x in off]
+    lay = eqb.run_layer(zt, bt, w.K, offl, fused=True)
+    H1 = torch.zeros_like(lay.hist_hi)
+    eqb.eqb_margin_hist_pass1(zt, lay.tau, H1, offl)
+    ld = torch.zeros_like(lay.load)
+    eqb.eqb_expert_load(lay.topk_idx, w.E, ld, offl)
+    torch.cuda.synchronize()
+    assert torch.equal(H1, lay.hist_hi)
+    assert torch.equal(ld, lay.load)
+
+
+def test_select_reports_rank_beyond_counts(eqb):
+    E = 8
+    say("select error status")
+    hist = torch.zeros((1, E, 256), dtype=torch.int32, device="cuda")
+    hist[0, :, 3] = 4                                   # four margins per expert
+    sel = torch.empty(E, dtype=torch.int32, device="cuda")
+    rib = torch.empty(E, dtype=torch.int64, device="cuda")
+    st = torch.zeros(1, dtype=torch.int32, device="cuda")
+    eqb.eqb_select_quantile(1, hist, 4, sel, rib, dev_status=st)
+    torch.cuda.synchronize()
+    assert st.item() == 0 and torch.all(sel == 3) and torch.all(rib == 4)
+    eqb.eqb_select_quantile(1, hist, 5, sel, rib, dev_status=st)
+    torch.cuda.synchronize()
+    assert st.item() == eqb.EQB_DEV_RANK_EXCEEDS_COUNT and torch.all(sel == -1)
+
+
+def test_bf16_rounding_of_every_high_half_through_both_passes(eqb):
+    """Margins tau - 0 = tau cover every finite high half with low halves at,
+    around and away from the tie point; the coarse counts and the fine counts
+    for every selected high byte must equal the oracle's, i.e. the device's
+    BF16 rounding and key agree with the oracle on this whole set."""
+    hi = np.arange(65536, dtype=np.uint32)
+    hi = hi[(hi & 0x7F80) < 0x7F00]                    # keep tau - 0 far from overflow
+    lows = np.array([0x0000, 0x0001, 0x7FFF, 0x8000, 0x8001, 0xFFFF, 0x4000, 0xC000], np.uint32)
+    tau = ((hi[:, None] << 16) | lows[None, :]).ravel().view(np.float32)
+    T, E = tau.size, 8
+    z = np.zeros((T, E), np.uint16)
+    z[:, 1] = 0x8000                                   # -0: tau - (-0) = tau as well
+    keys = O.margin_keys(z, tau)
+    say(f"rounding sweep T={T}")
+    zt = torch.from_numpy(z.view(np.int16)).cuda()
+    tt = torch.from_numpy(tau).cuda()
+    H = torch.zeros((1, E, 256), dtype=torch.int32, device="cuda")
+    eqb.eqb_margin_hist_pass1(zt, tt, H)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(H.cpu().numpy()[0], O.count_high(keys, [0, T])[0])
+    L = torch.zeros((1, E, 256), dtype=torch.int32, device="cuda")
+    for u in range(256):
+        sel = torch.full((E,), u, dtype=torch.int32, device="cuda")
+        L.zero_()
+        eqb.eqb_margin_hist_pass2(zt, tt, sel, L)
+        torch.cuda.synchronize()
+        want = O.count_low(keys[:, :2], np.array([u, u]), [0, T])[0]
+        np.testing.assert_array_equal(L.cpu().numpy()[0, :2], want, err_msg=f"u={u}")
