@@ -87,6 +87,9 @@ def main():
     ap.add_argument("--cpu-rows", type=int, default=262144,
                     help="tokens in the CPU-oracle baseline slice (0 disables it)")
     ap.add_argument("--stages", action="store_true", help="also print per-stage times to stderr")
+    ap.add_argument("--copy-calibration-mib", type=int, default=0,
+                    help="after the run, copy a device buffer of this size three times "
+                         "(a plain copy of known size, used to scale HBM counters)")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -185,6 +188,14 @@ def main():
         out["cpu_baseline"] = None
     if args.stages:
         print(json.dumps(stage_ms), file=sys.stderr)
+    if args.copy_calibration_mib > 0:
+        n = args.copy_calibration_mib << 20
+        src = torch.ones(n // 4, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(f"[bench] copied {n} bytes three times for counter calibration", file=sys.stderr)
     print(json.dumps(out), flush=True)
 
 

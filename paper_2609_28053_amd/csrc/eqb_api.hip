@@ -1,0 +1,148 @@
+// eqb_api.hip - the C ABI declared in include/eqb.h.  Every argument check
+// runs before anything is enqueued; the calls never synchronise the host.
+#include "eqb_internal.hpp"
+
+namespace eqb {
+
+int num_cus() {
+  static int cached[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (cached[dev] == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+    cached[dev] = n;
+  }
+  return cached[dev];
+}
+
+namespace {
+
+bool supported_E(int32_t E) { return E == 8 || E == 16 || E == 32 || E == 64 || E == 128 || E == 256; }
+
+eqb_status make_table(const int64_t* part_off, int32_t P, int64_t T, PartTable* pt) {
+  if (part_off == nullptr) {
+    if (P != 1) return EQB_ERR_INVALID_ARG;
+    pt->P = 1;
+    pt->off[0] = 0;
+    pt->off[1] = T;
+    return EQB_OK;
+  }
+  if (P < 1 || P > EQB_MAX_PARTITIONS) return EQB_ERR_INVALID_ARG;
+  if (part_off[0] != 0 || part_off[P] != T) return EQB_ERR_INVALID_ARG;
+  for (int p = 0; p < P; ++p)
+    if (part_off[p + 1] < part_off[p]) return EQB_ERR_INVALID_ARG;
+  pt->P = P;
+  for (int p = 0; p <= P; ++p) pt->off[p] = part_off[p];
+  return EQB_OK;
+}
+
+bool aligned16(const void* p) { return reinterpret_cast<uintptr_t>(p) % 16 == 0; }
+
+}  // namespace
+}  // namespace eqb
+
+using namespace eqb;
+
+extern "C" {
+
+eqb_status eqb_route_topk(const uint16_t* z, const float* b, int64_t T, int32_t E, int32_t K,
+                          int32_t* topk_idx, float* topk_score, float* tau,
+                          const int64_t* part_off, int32_t P,
+                          int32_t* load, int32_t* hist_hi, void* stream) {
+  if (T < 0 || T > INT32_MAX || K < 1 || K >= E) return EQB_ERR_INVALID_ARG;
+  if (!supported_E(E)) return EQB_ERR_UNSUPPORTED;
+  RouteArgs a;
+  const eqb_status st = make_table(part_off, P, T, &a.pt);
+  if (st != EQB_OK) return st;
+  if (T == 0) return EQB_OK;
+  if (!z || !b || !topk_idx || !topk_score || !tau) return EQB_ERR_INVALID_ARG;
+  if (!aligned16(z)) return EQB_ERR_UNSUPPORTED;
+  a.z = z;
+  a.b = b;
+  a.T = T;
+  a.E = E;
+  a.K = K;
+  a.idx = topk_idx;
+  a.score = topk_score;
+  a.tau = tau;
+  a.load = load;
+  a.hist = hist_hi;
+  return launch_route(a, static_cast<hipStream_t>(stream));
+}
+
+static eqb_status margin_pass(bool fine, const uint16_t* z, const float* tau, int64_t T, int32_t E,
+                              const int32_t* sel_hi, const int64_t* part_off, int32_t P, int32_t* hist,
+                              void* stream) {
+  if (T < 0 || T > INT32_MAX) return EQB_ERR_INVALID_ARG;
+  if (!supported_E(E)) return EQB_ERR_UNSUPPORTED;
+  MarginArgs a;
+  const eqb_status st = make_table(part_off, P, T, &a.pt);
+  if (st != EQB_OK) return st;
+  if (T == 0) return EQB_OK;
+  if (!z || !tau || !hist || (fine && !sel_hi)) return EQB_ERR_INVALID_ARG;
+  if (!aligned16(z)) return EQB_ERR_UNSUPPORTED;
+  a.z = z;
+  a.tau = tau;
+  a.T = T;
+  a.E = E;
+  a.sel_hi = sel_hi;
+  a.hist = hist;
+  return launch_margin(fine, a, static_cast<hipStream_t>(stream));
+}
+
+eqb_status eqb_margin_hist_pass1(const uint16_t* z, const float* tau, int64_t T, int32_t E,
+                                 const int64_t* part_off, int32_t P, int32_t* hist_hi, void* stream) {
+  return margin_pass(false, z, tau, T, E, nullptr, part_off, P, hist_hi, stream);
+}
+
+eqb_status eqb_margin_hist_pass2(const uint16_t* z, const float* tau, int64_t T, int32_t E,
+                                 const int32_t* sel_hi, const int64_t* part_off, int32_t P,
+                                 int32_t* hist_lo, void* stream) {
+  return margin_pass(true, z, tau, T, E, sel_hi, part_off, P, hist_lo, stream);
+}
+
+eqb_status eqb_select_quantile(int32_t pass, const int32_t* hist, int32_t P, int32_t E, int64_t r,
+                               int32_t* sel_hi, int64_t* rank_in_bin,
+                               int32_t* sel_lo, uint16_t* q_bf16, float* b_next,
+                               int32_t* hist_sum, int32_t* dev_status, void* stream) {
+  if (pass != 1 && pass != 2) return EQB_ERR_INVALID_ARG;
+  if (P < 1 || P > EQB_MAX_PARTITIONS) return EQB_ERR_INVALID_ARG;
+  if (!supported_E(E)) return EQB_ERR_UNSUPPORTED;
+  if (r < 1 || r > INT32_MAX) return EQB_ERR_RANK;
+  if (!hist || !sel_hi || !rank_in_bin) return EQB_ERR_INVALID_ARG;
+  if (pass == 2 && (!sel_lo || !q_bf16)) return EQB_ERR_INVALID_ARG;
+  return launch_select(pass, hist, P, E, r, sel_hi, rank_in_bin, sel_lo, q_bf16, b_next, hist_sum,
+                       dev_status, static_cast<hipStream_t>(stream));
+}
+
+eqb_status eqb_expert_load(const int32_t* topk_idx, int64_t T, int32_t K, int32_t E,
+                           const int64_t* part_off, int32_t P, int32_t* load, void* stream) {
+  if (T < 0 || T > INT32_MAX || K < 1 || K >= E) return EQB_ERR_INVALID_ARG;
+  if (!supported_E(E)) return EQB_ERR_UNSUPPORTED;
+  PartTable pt;
+  const eqb_status st = make_table(part_off, P, T, &pt);
+  if (st != EQB_OK) return st;
+  if (T == 0) return EQB_OK;
+  if (!topk_idx || !load) return EQB_ERR_INVALID_ARG;
+  return launch_load(topk_idx, T, K, E, load, pt, static_cast<hipStream_t>(stream));
+}
+
+int64_t eqb_rank(int64_t T_total, int32_t K, int32_t E) {
+  if (T_total < 0 || E < 1 || K < 1 || K >= E) return -1;
+  if (T_total > ((int64_t)1 << 40)) return -1;
+  return (T_total * (int64_t)K + E - 1) / E;
+}
+
+const char* eqb_status_string(eqb_status status) {
+  switch (status) {
+    case EQB_OK: return "EQB_OK";
+    case EQB_ERR_INVALID_ARG: return "EQB_ERR_INVALID_ARG";
+    case EQB_ERR_UNSUPPORTED: return "EQB_ERR_UNSUPPORTED";
+    case EQB_ERR_RANK: return "EQB_ERR_RANK";
+    case EQB_ERR_HIP: return "EQB_ERR_HIP";
+    default: return "EQB_ERR_UNKNOWN";
+  }
+}
+
+}  // extern "C"

@@ -1,0 +1,180 @@
+// eqb_device.hpp - device helpers shared by the gfx950 kernels of libeqb.
+//
+// Method: arXiv 2609.28053 (Exact Quantile Balancing), Sec. 2-3 and
+// Algorithm 1 of Appendix C.  Nothing in here is exported.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "eqb.h"
+
+namespace eqb {
+
+constexpr int kNBins = 256;
+constexpr int kBlock = 1024;            // threads of a streaming block
+constexpr int kWaves = kBlock / 64;
+constexpr int64_t kSegMax = 65535;      // rows per LDS histogram flush (16-bit counters)
+constexpr int kHistStride = kNBins + 1; // LDS words per expert pair (odd stride spreads banks)
+
+// Contiguous token partitions [off[p], off[p+1]), passed by value.
+struct PartTable {
+  int64_t off[EQB_MAX_PARTITIONS + 1];
+  int32_t P;
+};
+
+// ------------------------------------------------------------ BF16 ------
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
+
+// Raw high byte of bf16_rne(x) from the binary32 bits of x.  Round-half-up
+// and round-half-even only differ on an exact tie with an even last BF16 bit,
+// and then the carry cannot reach bit 24, so adding 0x8000 is exact here.
+__device__ __forceinline__ uint32_t bf16_raw_hi(uint32_t bits) { return (bits + 0x8000u) >> 24; }
+
+// kappa maps BF16 bits to an order-preserving key: negative patterns flip
+// every bit, non-negative ones only the sign.  On the raw high byte hr this
+// is hr ^ 0xFF (sign set) or hr ^ 0x80; on the raw low byte lr it is lr ^ 0xFF
+// for negative values and lr otherwise.
+__device__ __forceinline__ int kappa_hi_of_raw(int hr) { return hr ^ ((hr & 0x80) ? 0xFF : 0x80); }
+__device__ __forceinline__ int raw_hi_of_kappa(int u) { return u ^ ((u & 0x80) ? 0x80 : 0xFF); }
+
+__device__ __forceinline__ uint16_t kappa_inv(uint32_t key) {
+  return (uint16_t)((key & 0x8000u) ? (key ^ 0x8000u) : (key ^ 0xFFFFu));
+}
+
+__device__ __forceinline__ float sigmoid_f32(float x) {
+  if (x >= 0.0f) return 1.0f / (1.0f + expf(-x));
+  const float ex = expf(x);
+  return ex / (1.0f + ex);
+}
+
+// ------------------------------------------------------- exact 64-bit keys --
+// Unsigned key ordered like the binary32 value, with -0 and +0 equal.
+__device__ __forceinline__ uint32_t order_key(uint32_t u) {
+  u = (u == 0x80000000u) ? 0u : u;
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+__device__ __forceinline__ uint32_t order_key_inv(uint32_t k) {
+  return (k & 0x80000000u) ? (k & 0x7FFFFFFFu) : ~k;
+}
+// Exact candidate key: high word = order key of s; low word = (255-e) << 24 |
+// (s is -0) << 16 | BF16 bits of z.  Unique per row; larger = better rank;
+// equal scores favour the lower expert index.
+__device__ __forceinline__ uint64_t exact_key(uint32_t sbits, int e, uint32_t zbits) {
+  const uint32_t lo = ((uint32_t)(255 - e) << 24) | ((sbits == 0x80000000u) ? (1u << 16) : 0u) | zbits;
+  return ((uint64_t)order_key(sbits) << 32) | lo;
+}
+__device__ __forceinline__ int exact_key_expert(uint64_t k) { return 255 - (int)((uint32_t)k >> 24); }
+__device__ __forceinline__ uint32_t exact_key_z(uint64_t k) { return (uint32_t)k & 0xFFFFu; }
+__device__ __forceinline__ uint32_t exact_key_sbits(uint64_t k) {
+  if ((uint32_t)k & (1u << 16)) return 0x80000000u;
+  return order_key_inv((uint32_t)(k >> 32));
+}
+
+__device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t v, int mask) {
+  const uint32_t lo = __shfl_xor((unsigned int)v, mask);
+  const uint32_t hi = __shfl_xor((unsigned int)(v >> 32), mask);
+  return ((uint64_t)hi << 32) | lo;
+}
+
+// ------------------------------------------------ group reductions (DPP) --
+// Maximum over aligned groups of G lanes (G = 1, 2, 4, 8 or 16); every lane
+// of the group receives it.  quad_perm swaps within quads, the half-row and
+// row mirrors pair the two halves of 8- and 16-lane groups.
+template <int G>
+__device__ __forceinline__ int group_max_i32(int x) {
+  if constexpr (G >= 2) x = max(x, __builtin_amdgcn_update_dpp(0, x, 0xB1, 0xF, 0xF, false));
+  if constexpr (G >= 4) x = max(x, __builtin_amdgcn_update_dpp(0, x, 0x4E, 0xF, 0xF, false));
+  if constexpr (G >= 8) x = max(x, __builtin_amdgcn_update_dpp(0, x, 0x141, 0xF, 0xF, false));
+  if constexpr (G >= 16) x = max(x, __builtin_amdgcn_update_dpp(0, x, 0x140, 0xF, 0xF, false));
+  static_assert(G <= 16, "group reductions cover at most 16 lanes");
+  return x;
+}
+
+template <int G>
+__device__ __forceinline__ uint64_t group_max_u64(uint64_t m) {
+#pragma unroll
+  for (int off = 1; off < G; off <<= 1) {
+    const uint64_t o = shfl_xor_u64(m, off);
+    m = o > m ? o : m;
+  }
+  return m;
+}
+
+__device__ __forceinline__ int med3_i32(int a, int b, int c) {
+  int r;
+  asm volatile("v_med3_i32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
+  return r;
+}
+
+// ------------------------------------------------------- partition walk --
+// Calls f(p, s0, s1) for every piece of [r0, r1) lying in one partition and
+// holding at most kSegMax rows.  Uniform across the block.
+template <class F>
+__device__ __forceinline__ void for_each_segment(int64_t r0, int64_t r1, const PartTable& pt, F&& f) {
+  int p = 0;
+  int64_t t = r0;
+  while (t < r1) {
+    while (p < pt.P - 1 && pt.off[p + 1] <= t) ++p;
+    int64_t end = pt.off[p + 1] < r1 ? pt.off[p + 1] : r1;
+    if (end - t > kSegMax) end = t + kSegMax;
+    f(p, t, end);
+    t = end;
+  }
+}
+
+// ------------------------------------------- packed LDS histograms -------
+// Counters of experts 2m (low half) and 2m+1 (high half) share one 32-bit
+// word at m * kHistStride + bin.  Bins are RAW BF16 bytes; the flush maps them
+// to kappa bins.
+template <int E>
+constexpr int hist_words() { return (E / 2) * kHistStride; }
+
+// kFine = false: raw high byte -> kappa high byte (same map for every expert).
+// kFine = true : raw low byte  -> kappa low byte, flipped for experts whose
+//                selected coarse bin holds negative values (u_e < 0x80).
+template <int E, bool kFine>
+__device__ __forceinline__ void flush_hist(uint32_t* sh, int32_t* __restrict__ slab,
+                                           const int32_t* __restrict__ sel_hi) {
+  for (int w = threadIdx.x; w < hist_words<E>(); w += blockDim.x) {
+    const uint32_t c = sh[w];
+    if (c) {
+      const int pair = w / kHistStride;
+      const int raw = w - pair * kHistStride;
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const uint32_t n = h ? (c >> 16) : (c & 0xFFFFu);
+        if (n) {
+          const int e = 2 * pair + h;
+          int bin;
+          if (kFine) bin = (sel_hi[e] < 0x80) ? (raw ^ 0xFF) : raw;
+          else bin = kappa_hi_of_raw(raw);
+          atomicAdd(slab + e * kNBins + bin, (int32_t)n);
+        }
+      }
+      sh[w] = 0;
+    }
+  }
+}
+
+// Word offset of expert e's row in a packed histogram and its increment.
+__device__ __forceinline__ uint32_t hist_row(int e) { return (uint32_t)(e >> 1) * kHistStride; }
+__device__ __forceinline__ uint32_t hist_inc(int e) { return 1u << ((e & 1) * 16); }
+
+// Rows handled by block blockIdx.x.
+__device__ __forceinline__ void block_rows(int64_t T, int64_t rows_per_block, int64_t* r0, int64_t* r1) {
+  *r0 = (int64_t)blockIdx.x * rows_per_block;
+  *r1 = (*r0 + rows_per_block < T) ? *r0 + rows_per_block : T;
+}
+
+}  // namespace eqb
+
+namespace eqb {
+// Orders this wave's LDS writes before its later LDS reads by other lanes.
+__device__ __forceinline__ void lds_wave_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+}
+}  // namespace eqb

@@ -1,0 +1,57 @@
+// eqb_internal.hpp - launch interfaces between the C ABI shim and the kernels.
+#pragma once
+
+#include "eqb_device.hpp"
+
+namespace eqb {
+
+struct RouteArgs {
+  const uint16_t* z;
+  const float* b;
+  int64_t T;
+  int E, K;
+  int32_t* idx;
+  float* score;
+  float* tau;
+  int32_t* load;
+  int32_t* hist;
+  PartTable pt;
+};
+
+struct MarginArgs {
+  const uint16_t* z;
+  const float* tau;
+  int64_t T;
+  int E;
+  const int32_t* sel_hi;   // fine pass only
+  int32_t* hist;
+  PartTable pt;
+};
+
+eqb_status launch_route(const RouteArgs& a, hipStream_t s);
+eqb_status launch_margin(bool fine, const MarginArgs& a, hipStream_t s);
+eqb_status launch_load(const int32_t* idx, int64_t T, int K, int E, int32_t* load, const PartTable& pt,
+                       hipStream_t s);
+eqb_status launch_select(int pass, const int32_t* hist, int P, int E, int64_t r, int32_t* sel_hi,
+                         int64_t* rank_in_bin, int32_t* sel_lo, uint16_t* q_bf16, float* b_next,
+                         int32_t* hist_sum, int32_t* status, hipStream_t s);
+
+// Number of compute units of the current device (cached per device).
+int num_cus();
+
+// Blocks and rows per block for a streaming kernel over T rows that advances
+// rows_per_step rows per block step: at most blocks_per_cu blocks per CU,
+// each owning a contiguous range of whole steps.
+inline void grid_for(int64_t T, int rows_per_step, int blocks_per_cu, int* blocks, int64_t* rows_per_block) {
+  const int64_t max_blocks = (int64_t)num_cus() * blocks_per_cu;
+  const int64_t steps = (T + rows_per_step - 1) / rows_per_step;
+  int64_t nb = steps < max_blocks ? steps : max_blocks;
+  if (nb < 1) nb = 1;
+  const int64_t steps_per_block = (steps + nb - 1) / nb;
+  *rows_per_block = steps_per_block * rows_per_step;
+  *blocks = (int)((T + *rows_per_block - 1) / *rows_per_block);
+}
+
+inline eqb_status launch_status() { return hipGetLastError() == hipSuccess ? EQB_OK : EQB_ERR_HIP; }
+
+}  // namespace eqb
