@@ -178,3 +178,14 @@ __device__ __forceinline__ void lds_wave_sync() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
 }
 }  // namespace eqb
+
+namespace eqb {
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float float2_t __attribute__((ext_vector_type(2)));
+// Both values rounded to BF16 (nearest, ties to even) in one conversion; the
+// first lands in bits 0..15, the second in bits 16..31.
+__device__ __forceinline__ uint32_t bf16x2_bits(float a, float b) {
+  const float2_t f = {a, b};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f, bf16x2_t));
+}
+}  // namespace eqb

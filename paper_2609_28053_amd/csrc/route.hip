@@ -5,7 +5,8 @@
 // Fast kernel (K <= kFastKmax).  A row of E logits is spread over G lanes,
 // each holding N = E/G experts as N/4 8-byte pieces.  Per element it forms a
 // 32-bit key: the binary32 bits of s = z + b with the low byte replaced by
-// 255 - e, and keeps a sorted top-4 list of keys (one v_max + three v_med3).
+// 255 - e, and keeps a sorted list of its kList largest keys (one v_max and
+// kList-1 v_med3 per element).
 // K+2 extraction rounds then take the group maximum of the list heads with
 // DPP and pop the winner, refilling a lane whose list runs dry.  For a
 // positive tau, signed key order is score order except between scores that
@@ -20,13 +21,22 @@
 namespace eqb {
 
 constexpr int kRmax = 16;              // extracted ranks kept per row
+constexpr int kList = 6;               // sorted keys kept per lane
 constexpr int kFastKmax = kRmax - 2;
 
 template <int E> struct FastCfg { static constexpr int G = E >= 64 ? 8 : E / 8; };
 
-template <int E>
+// Insert x into the sorted list L[0] >= ... >= L[n-1] (one max, n-1 med3).
+template <int n>
+__device__ __forceinline__ void list_insert(int (&L)[n], int x) {
+#pragma unroll
+  for (int j = n - 1; j > 0; --j) L[j] = med3_i32(L[j - 1], L[j], x);
+  L[0] = max(L[0], x);
+}
+
+template <int E, int KT>
 __global__ __launch_bounds__(kBlock) void route_fast_kernel(
-    const uint16_t* __restrict__ z, const float* __restrict__ b, int64_t T, int K,
+    const uint16_t* __restrict__ z, const float* __restrict__ b, int64_t T, int Kdyn,
     int32_t* __restrict__ topk_idx, float* __restrict__ topk_score, float* __restrict__ tau,
     int32_t* __restrict__ load, int32_t* __restrict__ hist, const PartTable pt,
     int64_t rows_per_block) {
@@ -37,6 +47,8 @@ __global__ __launch_bounds__(kBlock) void route_fast_kernel(
   constexpr int ROWS = kWaves * R;      // rows per block step
   constexpr int RSLOT = (kRmax + G - 1) / G;
   static_assert(N % 4 == 0 && N >= 8, "layout");
+  static_assert(KT == 0 || KT + 2 <= E, "K+2 keys must exist");
+  const int K = KT > 0 ? KT : Kdyn;
 
   __shared__ uint32_t sh_hist[hist_words<E>()];
   __shared__ uint32_t sh_load[E];
@@ -52,6 +64,9 @@ __global__ __launch_bounds__(kBlock) void route_fast_kernel(
   auto ex = [&](int q) -> int { return q * 4 * G + g * 4; };
   // bytes 255 - e for the four experts of a piece (ex is a multiple of 4, no borrow)
   auto idxpk = [&](int q) -> uint32_t { return 0xFCFDFEFFu - (uint32_t)ex(q) * 0x01010101u; };
+  auto bias4 = [&](int q) -> float4 { return *reinterpret_cast<const float4*>(&sh_b[ex(q)]); };
+  auto pick = [](const float4& v, int i) -> float { return i == 0 ? v.x : i == 1 ? v.y : i == 2 ? v.z : v.w; };
+
   for (int w = threadIdx.x; w < hist_words<E>(); w += kBlock) sh_hist[w] = 0;
   for (int e = threadIdx.x; e < E; e += kBlock) {
     sh_load[e] = 0;
@@ -63,19 +78,287 @@ __global__ __launch_bounds__(kBlock) void route_fast_kernel(
   block_rows(T, rows_per_block, &r0, &r1);
   uint2* myrank = sh_rank[wave][r];
 
-  auto bias4 = [&](int q) -> float4 { return *reinterpret_cast<const float4*>(&sh_b[ex(q)]); };
-  auto key_of = [&](const uint2* raw, int q, int i, const float4& bq, uint32_t ipk) -> int {
-    const uint32_t w = (i < 2) ? raw[q].x : raw[q].y;
-    const float zf = (i & 1) ? bf16_hi(w) : bf16_lo(w);
-    const float bv = i == 0 ? bq.x : i == 1 ? bq.y : i == 2 ? bq.z : bq.w;
+  // key of element (q, i) from its widened logit
+  auto key_of = [&](float zf, float bv, uint32_t ipk, int i) -> int {
     const uint32_t sb = __float_as_uint(zf + bv);
     return (int)__builtin_amdgcn_perm(sb, ipk, 0x07060500u | (uint32_t)i);
   };
 
-  for_each_segment(r0, r1, pt, [&](int p, int64_t s0, int64_t s1) {
-    uint2 raw[NQ], nxt[NQ];
+  // Rebuild a lane's sorted list from its keys strictly below thr.
+  auto rebuild = [&](const float (&zf)[N], int thr, int (&L)[kList]) __attribute__((always_inline)) {
 #pragma unroll
-    for (int q = 0; q < NQ; ++q) nxt[q] = make_uint2(0, 0);
+    for (int j = 0; j < kList; ++j) L[j] = INT_MIN;
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) {
+      const float4 bq = bias4(q);
+      const uint32_t ipk = idxpk(q);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int x = key_of(zf[q * 4 + i], pick(bq, i), ipk, i);
+        list_insert(L, (x < thr) ? x : INT_MIN);
+      }
+    }
+  };
+
+  auto process = [&](const uint2 (&raw)[NQ], int64_t t, bool valid) __attribute__((always_inline)) {
+    // ---- widen the logits once; build keys and the per-lane sorted list
+    float zf[N];
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) {
+      zf[q * 4 + 0] = bf16_lo(raw[q].x);
+      zf[q * 4 + 1] = bf16_hi(raw[q].x);
+      zf[q * 4 + 2] = bf16_lo(raw[q].y);
+      zf[q * 4 + 3] = bf16_hi(raw[q].y);
+    }
+    int L[kList];
+#pragma unroll
+    for (int j = 0; j < kList; ++j) L[j] = INT_MIN;
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) {
+      const float4 bq = bias4(q);
+      const uint32_t ipk = idxpk(q);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) list_insert(L, key_of(zf[q * 4 + i], pick(bq, i), ipk, i));
+    }
+
+    // ---- extraction rounds: group maximum of the list heads, winner pops
+    auto pop = [&](int M) {
+      const bool win = (L[0] == M);
+#pragma unroll
+      for (int j = 0; j < kList - 1; ++j) L[j] = win ? L[j + 1] : L[j];
+      L[kList - 1] = win ? INT_MIN : L[kList - 1];
+    };
+    // Rows whose ranks are staged in LDS: run past rank K+1, equal top-24-bit
+    // keys, a list that ran dry, or (slow) a cutoff that is not positive.
+    bool staged = false, slow = false;
+    int nrank = 0;
+    float tv = 0.0f;          // tau of this lane's row (common rows)
+    int rk[RSLOT];
+#pragma unroll
+    for (int s = 0; s < RSLOT; ++s) rk[s] = INT_MIN;
+
+    if constexpr (KT > 0) {
+      int mK = INT_MIN, mK1 = INT_MIN, prev = INT_MIN;
+      bool near = false;      // two adjacent extracted keys share their top 24 bits
+#pragma unroll
+      for (int k = 0; k < KT + 2; ++k) {
+        const int M = group_max_i32<G>(L[0]);
+        if (k < KT + 1) pop(M);
+        rk[k / G] = (g == k % G) ? M : rk[k / G];
+        if (k > 0) near |= ((uint32_t)(M ^ prev) < 256u);
+        prev = M;
+        if (k == KT) mK = M;
+        if (k == KT + 1) mK1 = M;
+      }
+      const int tauhi = mK >> 8;
+      const bool dry = group_max_i32<G>((int)(L[0] == INT_MIN)) != 0;
+      slow = valid && tauhi <= 0;
+      staged = valid && !slow && (near || dry);
+      nrank = KT + 2;
+      if (__any(staged)) {
+        // stage the keys, extend the run of rank K if it continues, then exact scores
+#pragma unroll
+        for (int s = 0; s < RSLOT; ++s) {
+          const int k = s * G + g;
+          if (staged && k < KT + 2) myrank[k].x = (uint32_t)rk[s];
+        }
+        // rank K+1 is still at the head of its list; keep extracting while
+        // the keys share the top 24 bits of rank K
+        bool ext = staged && !dry && (mK1 >> 8) == tauhi;
+        bool bad = false;           // row-uniform: extraction can no longer be trusted
+        if (__any(ext)) {
+          pop(mK1);
+          for (int k = KT + 2; k < kRmax; ++k) {
+            if (!__any(ext)) break;
+            // a lane whose list ran dry may hold the next key
+            const bool dry_now = group_max_i32<G>((int)(L[0] == INT_MIN)) != 0;
+            if (ext && dry_now) {
+              bad = true;
+              ext = false;
+            }
+            const int M = group_max_i32<G>(L[0]);
+            if (ext) {
+              if (g == 0) myrank[k].x = (uint32_t)M;
+              nrank = k + 1;
+              if ((M >> 8) != tauhi) ext = false;
+            }
+            pop(M);
+          }
+        }
+        bad = bad || ext;           // the run is longer than the rank buffer
+        slow = slow || bad || (staged && dry);
+        staged = staged && !slow;
+        lds_wave_sync();
+#pragma unroll
+        for (int s = 0; s < RSLOT; ++s) {
+          const int k = s * G + g;
+          if (staged && k < nrank) {
+            const int e = 255 - (int)(myrank[k].x & 0xFF);
+            const uint32_t zb = z[t * E + e];
+            const uint32_t sb = __float_as_uint(__uint_as_float(zb << 16) + sh_b[e]);
+            myrank[k] = make_uint2(sb, (zb << 16) | (uint32_t)e);
+          }
+        }
+        lds_wave_sync();
+      }
+    } else {
+      bool done = !valid;
+      int tauhi = 0;
+#pragma unroll 1
+      for (int k = 0; k < kRmax; ++k) {
+        if (!__any(!done)) break;
+        const int M = group_max_i32<G>(L[0]);
+        pop(M);
+        const bool dry = (L[0] == INT_MIN) && (M != INT_MIN);
+        if (__any(dry && !done)) {
+          if (dry && !done) rebuild(zf, M, L);
+        }
+        if (!done) {
+          if (M == INT_MIN) {
+            done = true;
+          } else {
+            if (g == 0) myrank[k].x = (uint32_t)M;
+            nrank = k + 1;
+            if (k == K) tauhi = M >> 8;
+            if (k > K && (M >> 8) != tauhi) done = true;   // one key past the run of rank K
+          }
+        }
+      }
+      slow = valid && (!done || tauhi <= 0);
+      staged = valid && !slow;
+      lds_wave_sync();
+#pragma unroll
+      for (int s = 0; s < RSLOT; ++s) {
+        const int k = s * G + g;
+        if (staged && k < nrank) {
+          const int e = 255 - (int)(myrank[k].x & 0xFF);
+          const uint32_t zb = z[t * E + e];
+          const uint32_t sb = __float_as_uint(__uint_as_float(zb << 16) + sh_b[e]);
+          myrank[k] = make_uint2(sb, (zb << 16) | (uint32_t)e);
+        }
+      }
+      lds_wave_sync();
+    }
+
+    // ---- staged rows: sort the extracted ranks exactly where top-24-bit keys tie
+    if (__any(staged)) {
+      bool coll = false;
+#pragma unroll
+      for (int s = 0; s < RSLOT; ++s) {
+        const int k = s * G + g;
+        if (staged && k + 1 < nrank) {
+          const uint2 a = myrank[k], c = myrank[k + 1];
+          coll |= ((a.x >> 8) == (c.x >> 8)) && (a.x != c.x);
+        }
+      }
+      const bool coll_row = group_max_i32<G>((int)coll) != 0;
+      if (coll_row && g == 0) {
+        for (int i = 1; i < nrank; ++i) {
+          const uint2 v = myrank[i];
+          int j = i - 1;
+          while (j >= 0) {
+            const uint2 u = myrank[j];
+            const bool worse = ((int)u.x < (int)v.x) || (u.x == v.x && (u.y & 0xFF) > (v.y & 0xFF));
+            if (!worse) break;
+            myrank[j + 1] = u;
+            --j;
+          }
+          myrank[j + 1] = v;
+        }
+      }
+      lds_wave_sync();
+    }
+
+    // ---- exact 64-bit extraction for rows flagged slow
+    if (__any(slow)) {
+      if (slow) {
+        uint64_t prevk = ~0ull;
+        for (int k = 0; k <= K; ++k) {
+          uint64_t m = 0;
+#pragma unroll
+          for (int q = 0; q < NQ; ++q) {
+            const float4 bq = bias4(q);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              // rebuilt every round instead of being held in 2*N registers
+              float zq = zf[q * 4 + i];
+              asm volatile("" : "+v"(zq));
+              const uint32_t zb = __float_as_uint(zq) >> 16;
+              const uint32_t sb = __float_as_uint(zq + pick(bq, i));
+              const uint64_t key = exact_key(sb, ex(q) + i, zb);
+              m = (key < prevk && key > m) ? key : m;
+            }
+          }
+          m = group_max_u64<G>(m);
+          prevk = m;
+          if (g == 0)
+            myrank[k] = make_uint2(exact_key_sbits(m), (exact_key_z(m) << 16) | (uint32_t)exact_key_expert(m));
+        }
+      }
+      lds_wave_sync();
+    }
+
+    // ---- outputs: ranks 0..K-1, loads, tau
+    const bool fromlds = staged || slow;
+    if (KT > 0 && valid && !fromlds) {
+      // rank k is held by lane k % G in slot k / G; its exact score is z + b of that expert
+      float tk = 0.0f;
+#pragma unroll
+      for (int s = 0; s < RSLOT; ++s) {
+        const int k = s * G + g;
+        if (k <= K) {
+          const int e = 255 - (rk[s] & 0xFF);
+          const uint32_t zb = z[t * E + e];
+          if (k < K) {
+            topk_idx[t * K + k] = e;
+            topk_score[t * K + k] = sigmoid_f32(__uint_as_float(zb << 16));
+            if (load) atomicAdd(&sh_load[e], 1u);
+          } else {
+            tk = __uint_as_float(zb << 16) + sh_b[e];
+          }
+        }
+      }
+      tv = tk;
+    }
+    if (KT > 0) {
+      // every lane of the row takes tau from the lane holding rank K
+      const int src = (lane - g) + (K % G);
+      tv = __shfl(tv, src);
+    }
+    if (valid && fromlds) {
+#pragma unroll
+      for (int s = 0; s < RSLOT; ++s) {
+        const int k = s * G + g;
+        if (k < K) {
+          const uint2 v = myrank[k];
+          const int e = (int)(v.y & 0xFF);
+          topk_idx[t * K + k] = e;
+          topk_score[t * K + k] = sigmoid_f32(__uint_as_float((v.y >> 16) << 16));
+          if (load) atomicAdd(&sh_load[e], 1u);
+        }
+      }
+      tv = __uint_as_float(myrank[K].x);
+    }
+    if (valid && g == 0) tau[t] = tv;
+
+    // ---- coarse counts: raw high byte of bf16(tau - z), two margins per conversion
+    if (hist && valid) {
+#pragma unroll
+      for (int q = 0; q < NQ; ++q) {
+        const uint32_t row = hist_row(ex(q));
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const uint32_t p = bf16x2_bits(tv - zf[q * 4 + 2 * h], tv - zf[q * 4 + 2 * h + 1]);
+          atomicAdd(&sh_hist[row + h * kHistStride + ((p >> 8) & 0xFFu)], 1u);
+          atomicAdd(&sh_hist[row + h * kHistStride + (p >> 24)], 1u << 16);
+        }
+      }
+    }
+    __builtin_amdgcn_wave_barrier();
+  };
+
+  for_each_segment(r0, r1, pt, [&](int p, int64_t s0, int64_t s1) {
+    uint2 bufa[NQ], bufb[NQ];
     auto load_rows = [&](uint2* dst, int64_t base) {
       const int64_t t = base + wave * R + r;
 #pragma unroll
@@ -86,183 +369,13 @@ __global__ __launch_bounds__(kBlock) void route_fast_kernel(
         for (int q = 0; q < NQ; ++q) dst[q] = row[ex(q) >> 2];
       }
     };
-    load_rows(raw, s0);
+    // the next step's loads are in flight while a step is processed
+    load_rows(bufa, s0);
     for (int64_t base = s0; base < s1; base += ROWS) {
-      if (base + ROWS < s1) load_rows(nxt, base + ROWS);
-      const int64_t t = base + wave * R + r;
-      const bool valid = t < s1;
-
-      // ---- per-lane sorted top-4 of keys
-      int la = INT_MIN, lb = INT_MIN, lc = INT_MIN, ld = INT_MIN;
+      if (base + ROWS < s1) load_rows(bufb, base + ROWS);
+      process(bufa, base + wave * R + r, base + wave * R + r < s1);
 #pragma unroll
-      for (int q = 0; q < NQ; ++q) {
-        const float4 bq = bias4(q);
-        const uint32_t ipk = idxpk(q);
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int x = key_of(raw, q, i, bq, ipk);
-          ld = med3_i32(lc, ld, x);
-          lc = med3_i32(lb, lc, x);
-          lb = med3_i32(la, lb, x);
-          la = max(la, x);
-        }
-      }
-
-      // ---- extraction rounds (group-uniform M); lane 0 of the group stages
-      // the key of rank k in myrank[k].x
-      bool done = !valid;
-      int nrank = 0, tauhi = 0;
-#pragma unroll 1
-      for (int k = 0; k < kRmax; ++k) {
-        if (!__any(!done)) break;
-        const int M = group_max_i32<G>(la);
-        const bool win = (la == M) && (M != INT_MIN);
-        if (win) {
-          la = lb;
-          lb = lc;
-          lc = ld;
-          ld = INT_MIN;
-        }
-        if (!done) {
-          if (M == INT_MIN) {           // no keys left in the row
-            done = true;
-          } else {
-            if (g == 0) myrank[k].x = (uint32_t)M;
-            nrank = k + 1;
-            if (k == K) tauhi = M >> 8;
-            if (k > K && (M >> 8) != tauhi) done = true;   // one key past the run of rank K
-          }
-        }
-        const bool need = win && la == INT_MIN && !done;
-        if (__any(need)) {
-          if (need) {   // rebuild this lane's list from its keys below M
-            lb = lc = ld = INT_MIN;
-#pragma unroll
-            for (int q = 0; q < NQ; ++q) {
-              const float4 bq = bias4(q);
-              const uint32_t ipk = idxpk(q);
-#pragma unroll
-              for (int i = 0; i < 4; ++i) {
-                int x = key_of(raw, q, i, bq, ipk);
-                x = (x < M) ? x : INT_MIN;
-                ld = med3_i32(lc, ld, x);
-                lc = med3_i32(lb, lc, x);
-                lb = med3_i32(la, lb, x);
-                la = max(la, x);
-              }
-            }
-          }
-        }
-      }
-      // exact path when tau is not a positive score or the run did not end
-      const bool slow = valid && (!done || tauhi <= 0);
-      lds_wave_sync();
-
-      // ---- owners replace the staged keys of their ranks by exact scores
-#pragma unroll
-      for (int s = 0; s < RSLOT; ++s) {
-        const int k = s * G + g;
-        if (valid && !slow && k < nrank) {
-          const int e = 255 - (int)(myrank[k].x & 0xFF);
-          const uint32_t zb = z[t * E + e];
-          const uint32_t sb = __float_as_uint(__uint_as_float(zb << 16) + sh_b[e]);
-          myrank[k] = make_uint2(sb, (zb << 16) | (uint32_t)e);
-        }
-      }
-      lds_wave_sync();
-
-      // ---- equal top-24-bit keys whose exact scores differ: sort the row exactly
-      bool coll = false;
-#pragma unroll
-      for (int s = 0; s < RSLOT; ++s) {
-        const int k = s * G + g;
-        if (valid && !slow && k + 1 < nrank) {
-          const uint2 a = myrank[k], c = myrank[k + 1];
-          coll |= ((a.x >> 8) == (c.x >> 8)) && (a.x != c.x);
-        }
-      }
-      const bool coll_row = group_max_i32<G>((int)coll) != 0;
-      if (__any(coll_row)) {
-        if (coll_row && g == 0) {
-          for (int i = 1; i < nrank; ++i) {
-            const uint2 v = myrank[i];
-            int j = i - 1;
-            while (j >= 0) {
-              const uint2 u = myrank[j];
-              const bool worse = ((int)u.x < (int)v.x) || (u.x == v.x && (u.y & 0xFF) > (v.y & 0xFF));
-              if (!worse) break;
-              myrank[j + 1] = u;
-              --j;
-            }
-            myrank[j + 1] = v;
-          }
-        }
-        lds_wave_sync();
-      }
-
-      // ---- exact 64-bit extraction for rows flagged slow
-      if (__any(slow)) {
-        if (slow) {
-          uint64_t prev = ~0ull;
-          for (int k = 0; k <= K; ++k) {
-            uint64_t m = 0;
-#pragma unroll
-            for (int q = 0; q < NQ; ++q) {
-              const float4 bq = bias4(q);
-              // keys are rebuilt every round instead of being held in 2*N registers
-              uint2 rq = raw[q];
-              asm volatile("" : "+v"(rq.x), "+v"(rq.y));
-#pragma unroll
-              for (int i = 0; i < 4; ++i) {
-                const uint32_t w = (i < 2) ? rq.x : rq.y;
-                const uint32_t zb = (i & 1) ? (w >> 16) : (w & 0xFFFFu);
-                const float bv = i == 0 ? bq.x : i == 1 ? bq.y : i == 2 ? bq.z : bq.w;
-                const uint32_t sb = __float_as_uint(__uint_as_float(zb << 16) + bv);
-                const uint64_t key = exact_key(sb, ex(q) + i, zb);
-                m = (key < prev && key > m) ? key : m;
-              }
-            }
-            m = group_max_u64<G>(m);
-            prev = m;
-            if (g == 0)
-              myrank[k] = make_uint2(exact_key_sbits(m), (exact_key_z(m) << 16) | (uint32_t)exact_key_expert(m));
-          }
-        }
-        lds_wave_sync();
-      }
-
-      // ---- outputs: ranks 0..K-1, loads, tau
-#pragma unroll
-      for (int s = 0; s < RSLOT; ++s) {
-        const int k = s * G + g;
-        if (valid && k < K) {
-          const uint2 v = myrank[k];
-          const int e = (int)(v.y & 0xFF);
-          topk_idx[t * K + k] = e;
-          topk_score[t * K + k] = sigmoid_f32(__uint_as_float((v.y >> 16) << 16));
-          if (load) atomicAdd(&sh_load[e], 1u);
-        }
-      }
-      const float tv = __uint_as_float(myrank[K].x);
-      if (valid && g == 0) tau[t] = tv;
-
-      // ---- coarse counts: raw high byte of bf16(tau - z) per expert
-      if (hist && valid) {
-#pragma unroll
-        for (int q = 0; q < NQ; ++q) {
-          const uint32_t row = hist_row(ex(q));
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const uint32_t w = (i < 2) ? raw[q].x : raw[q].y;
-            const float zf = (i & 1) ? bf16_hi(w) : bf16_lo(w);
-            const uint32_t hr = bf16_raw_hi(__float_as_uint(tv - zf));
-            atomicAdd(&sh_hist[row + (i >> 1) * kHistStride + hr], 1u << ((i & 1) * 16));
-          }
-        }
-      }
-      __builtin_amdgcn_wave_barrier();
-#pragma unroll
-      for (int q = 0; q < NQ; ++q) raw[q] = nxt[q];
+      for (int q = 0; q < NQ; ++q) bufa[q] = bufb[q];
     }
     __syncthreads();
     if (hist) flush_hist<E, false>(sh_hist, hist + (int64_t)p * E * kNBins, nullptr);
@@ -356,15 +469,33 @@ __global__ __launch_bounds__(kBlock) void route_generic_kernel(
 }
 
 // ------------------------------------------------------------- launch ---
-template <int E>
-eqb_status launch_route_e(const RouteArgs& a, hipStream_t s) {
+template <int E, int KT>
+void launch_fast(const RouteArgs& a, hipStream_t s) {
   int blocks;
   int64_t rpb;
+  grid_for(a.T, kWaves * (64 / FastCfg<E>::G), 1, &blocks, &rpb);
+  route_fast_kernel<E, KT><<<blocks, kBlock, 0, s>>>(a.z, a.b, a.T, a.K, a.idx, a.score, a.tau, a.load,
+                                                     a.hist, a.pt, rpb);
+}
+
+template <int E>
+eqb_status launch_route_e(const RouteArgs& a, hipStream_t s) {
   if (a.K <= kFastKmax) {
-    grid_for(a.T, kWaves * (64 / FastCfg<E>::G), 1, &blocks, &rpb);
-    route_fast_kernel<E><<<blocks, kBlock, 0, s>>>(a.z, a.b, a.T, a.K, a.idx, a.score, a.tau, a.load,
-                                                   a.hist, a.pt, rpb);
+    // the common MoE fan-outs get a kernel with the rounds unrolled
+    if constexpr (E >= 64) {
+      switch (a.K) {
+        case 1: launch_fast<E, 1>(a, s); return launch_status();
+        case 2: launch_fast<E, 2>(a, s); return launch_status();
+        case 4: launch_fast<E, 4>(a, s); return launch_status();
+        case 6: launch_fast<E, 6>(a, s); return launch_status();
+        case 8: launch_fast<E, 8>(a, s); return launch_status();
+        default: break;
+      }
+    }
+    launch_fast<E, 0>(a, s);
   } else {
+    int blocks;
+    int64_t rpb;
     grid_for(a.T, kWaves * (64 / (E / 8)), 1, &blocks, &rpb);
     route_generic_kernel<E><<<blocks, kBlock, 0, s>>>(a.z, a.b, a.T, a.K, a.idx, a.score, a.tau, a.load,
                                                       a.hist, a.pt, rpb);
