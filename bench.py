@@ -27,7 +27,7 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0                     # MI355X HBM3E, vendor figure
 METRIC = "routing+EQB tokens/s per MoE layer; achieved HBM GB/s vs peak"
-SRC = os.path.join(ROOT, "paper_2609_28053_amd", "csrc", "eqb.hip")
+CSRC = os.path.join(ROOT, "paper_2609_28053_amd", "csrc")
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "route_hist1_large256_traffic.txt")
 
 
@@ -42,8 +42,12 @@ def pass_bytes_per_token(E, K):
 
 
 def source_hash():
-    with open(SRC, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+    """Hash of every kernel source; counters taken on other sources are stale."""
+    h = hashlib.sha256()
+    for name in sorted(os.listdir(CSRC)):
+        with open(os.path.join(CSRC, name), "rb") as f:
+            h.update(name.encode() + b"\0" + f.read())
+    return h.hexdigest()[:16]
 
 
 def read_traffic(T):
@@ -84,13 +88,17 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="large256")
-    ap.add_argument("--cpu-rows", type=int, default=262144,
+    ap.add_argument("--cpu-rows", type=int, default=1048576,
                     help="tokens in the CPU-oracle baseline slice (0 disables it)")
     ap.add_argument("--stages", action="store_true", help="also print per-stage times to stderr")
+    ap.add_argument("--print-source-hash", action="store_true", help="print the kernel source hash and exit")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="after the run, copy a device buffer of this size three times "
                          "(a plain copy of known size, used to scale HBM counters)")
     args = ap.parse_args()
+    if args.print_source_hash:
+        print(source_hash())
+        return
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: this build has no multi-GPU path "

@@ -49,6 +49,26 @@ __device__ __forceinline__ float sigmoid_f32(float x) {
   return ex / (1.0f + ex);
 }
 
+// sigmoid(x) = 1 / (1 + e) for x >= 0 and e / (1 + e) for x < 0, with
+// e = exp(-|x|) = 2^(-|x| log2 e).  The product |x| log2 e is carried as
+// p_hi + p_lo (log2 e split into two binary32 parts, the rounding error of
+// the leading product recovered with an fma), 2^(-p_hi) comes from the
+// hardware exponential and 2^(-p_lo) ~ 1 - p_lo ln 2 corrects it.  Relative
+// error stays within a few ulp for |x| <= 64; larger |x| use the libm path.
+__device__ __forceinline__ float sigmoid_fast(float x) {
+  const float a = fabsf(x);
+  if (a > 64.0f) return sigmoid_f32(x);
+  const float kLog2eHi = 1.44269502162933349609375f;   // binary32 nearest to log2(e)
+  const float kLog2eLo = 1.925963033500011e-08f;       // log2(e) - kLog2eHi
+  const float kLn2 = 0.693147180559945309f;
+  const float p_hi = a * kLog2eHi;
+  const float p_lo = __builtin_fmaf(a, kLog2eLo, __builtin_fmaf(a, kLog2eHi, -p_hi));
+  const float e1 = __builtin_amdgcn_exp2f(-p_hi);
+  const float e = __builtin_fmaf(-e1, p_lo * kLn2, e1);
+  const float r = __builtin_amdgcn_rcpf(1.0f + e);
+  return x >= 0.0f ? r : e * r;
+}
+
 // ------------------------------------------------------- exact 64-bit keys --
 // Unsigned key ordered like the binary32 value, with -0 and +0 equal.
 __device__ __forceinline__ uint32_t order_key(uint32_t u) {

@@ -26,6 +26,22 @@ constexpr int kFastKmax = kRmax - 2;
 
 template <int E> struct FastCfg { static constexpr int G = E >= 64 ? 8 : E / 8; };
 
+// The BF16 logit z of an extracted key.  The key holds the top 24 bits H of
+// s = fl32(z + b) (low byte = expert index).  When |z| >= |s| / 64, two
+// adjacent BF16 values give scores more than 256 binary32 ulps of s apart,
+// so at most one BF16 value maps to H; it is bf16(s_mid - b) with s_mid the
+// middle of the 256-ulp interval, and it is accepted only after
+// fl32(z + b) is checked to reproduce H.  Otherwise z is read from memory.
+__device__ __forceinline__ uint32_t z_from_key(int key, float b, const uint16_t* zptr) {
+  const uint32_t kb = (uint32_t)key;
+  const float s_mid = __uint_as_float((kb & 0xFFFFFF00u) | 0x80u);
+  const uint32_t zc = bf16x2_bits(s_mid - b, 0.0f) & 0xFFFFu;
+  const uint32_t sc = __float_as_uint(__uint_as_float(zc << 16) + b);
+  const int ez = (int)((zc >> 7) & 0xFFu), es = (int)((kb >> 23) & 0xFFu);
+  const bool ok = ((sc ^ kb) < 256u) && (ez >= es - 6) && ((zc & 0x7F80u) != 0x7F80u);
+  return ok ? zc : (uint32_t)*zptr;
+}
+
 // Insert x into the sorted list L[0] >= ... >= L[n-1] (one max, n-1 med3).
 template <int n>
 __device__ __forceinline__ void list_insert(int (&L)[n], int x) {
@@ -134,8 +150,12 @@ __global__ __launch_bounds__(kBlock) void route_fast_kernel(
     int nrank = 0;
     float tv = 0.0f;          // tau of this lane's row (common rows)
     int rk[RSLOT];
+    uint32_t zown[RSLOT];
 #pragma unroll
-    for (int s = 0; s < RSLOT; ++s) rk[s] = INT_MIN;
+    for (int s = 0; s < RSLOT; ++s) {
+      rk[s] = INT_MIN;
+      zown[s] = 0;
+    }
 
     if constexpr (KT > 0) {
       int mK = INT_MIN, mK1 = INT_MIN, prev = INT_MIN;
@@ -149,6 +169,15 @@ __global__ __launch_bounds__(kBlock) void route_fast_kernel(
         prev = M;
         if (k == KT) mK = M;
         if (k == KT + 1) mK1 = M;
+      }
+      // z of the experts at this lane's ranks, recovered from their keys
+#pragma unroll
+      for (int s = 0; s < RSLOT; ++s) {
+        const int k = s * G + g;
+        if (valid && k <= KT) {
+          const int e = 255 - (rk[s] & 0xFF);
+          zown[s] = z_from_key(rk[s], sh_b[e], z + t * E + e);
+        }
       }
       const int tauhi = mK >> 8;
       const bool dry = group_max_i32<G>((int)(L[0] == INT_MIN)) != 0;
@@ -193,9 +222,11 @@ __global__ __launch_bounds__(kBlock) void route_fast_kernel(
         for (int s = 0; s < RSLOT; ++s) {
           const int k = s * G + g;
           if (staged && k < nrank) {
-            const int e = 255 - (int)(myrank[k].x & 0xFF);
-            const uint32_t zb = z[t * E + e];
-            const uint32_t sb = __float_as_uint(__uint_as_float(zb << 16) + sh_b[e]);
+            const int key = (int)myrank[k].x;
+            const int e = 255 - (key & 0xFF);
+            const float bv = sh_b[e];
+            const uint32_t zb = z_from_key(key, bv, z + t * E + e);
+            const uint32_t sb = __float_as_uint(__uint_as_float(zb << 16) + bv);
             myrank[k] = make_uint2(sb, (zb << 16) | (uint32_t)e);
           }
         }
@@ -308,10 +339,10 @@ __global__ __launch_bounds__(kBlock) void route_fast_kernel(
         const int k = s * G + g;
         if (k <= K) {
           const int e = 255 - (rk[s] & 0xFF);
-          const uint32_t zb = z[t * E + e];
+          const uint32_t zb = zown[s];
           if (k < K) {
             topk_idx[t * K + k] = e;
-            topk_score[t * K + k] = sigmoid_f32(__uint_as_float(zb << 16));
+            topk_score[t * K + k] = sigmoid_fast(__uint_as_float(zb << 16));
             if (load) atomicAdd(&sh_load[e], 1u);
           } else {
             tk = __uint_as_float(zb << 16) + sh_b[e];
@@ -333,7 +364,7 @@ __global__ __launch_bounds__(kBlock) void route_fast_kernel(
           const uint2 v = myrank[k];
           const int e = (int)(v.y & 0xFF);
           topk_idx[t * K + k] = e;
-          topk_score[t * K + k] = sigmoid_f32(__uint_as_float((v.y >> 16) << 16));
+          topk_score[t * K + k] = sigmoid_fast(__uint_as_float((v.y >> 16) << 16));
           if (load) atomicAdd(&sh_load[e], 1u);
         }
       }
