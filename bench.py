@@ -68,6 +68,16 @@ def read_traffic(T):
         return None
 
 
+def cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown CPU"
+
+
 def cpu_baseline(w, rows, threads=1):
     import workloads as W
     from oracle import eqb_oracle as O
@@ -79,7 +89,7 @@ def cpu_baseline(w, rows, threads=1):
     return {"value": rows / dt, "unit": "tokens/s", "cores": threads, "kind": "oracle",
             "sample": f"first {rows} tokens of {w.name} (E={w.E}, K={w.K}, one partition), "
                       f"full oracle layer (row sorts, margins, column sorts, counts) in "
-                      f"{dt:.1f} s on {threads} thread(s) of {os.cpu_count()} visible cores"}
+                      f"{dt:.1f} s on {threads} thread(s) of {os.cpu_count()} visible cores ({cpu_model()})"}
 
 
 def main():
@@ -161,6 +171,9 @@ def main():
     stage_ms = {n: float(np.mean([evs[i][j].elapsed_time(evs[i][j + 1]) for i in range(args.steps)]))
                 for j, n in enumerate(names)}
     ms_per_step = elapsed * 1e3 / args.steps
+    per_step = np.array([evs[i][0].elapsed_time(evs[i][5]) for i in range(args.steps)])
+    step_ms = {"median": float(np.median(per_step)), "min": float(per_step.min()),
+               "p90": float(np.percentile(per_step, 90))}
     tokens_per_s = w.T / (ms_per_step * 1e-3)
     pass_gbs = pass_bytes_per_token(w.E, w.K) * w.T / (ms_per_step * 1e-3) / 1e9
     route_bytes = route_bytes_per_token(w.E, w.K) * w.T
@@ -186,6 +199,7 @@ def main():
         "pass_hbm_gbs": pass_gbs,
         "pass_frac_of_peak": pass_gbs / HBM_PEAK_GBS,
         "stage_ms": stage_ms,
+        "step_ms_events": step_ms,
         "roofline": {"kernel": "route_hist1", "bound": "hbm", "achieved": route_gbs,
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": route_gbs / HBM_PEAK_GBS,
                      "traffic": traffic, "algorithmic_bytes": route_bytes},
