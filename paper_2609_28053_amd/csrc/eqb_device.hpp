@@ -144,6 +144,20 @@ __device__ __forceinline__ void for_each_segment(int64_t r0, int64_t r1, const P
   }
 }
 
+// The same pieces in reverse order (last rows first).
+template <class F>
+__device__ __forceinline__ void for_each_segment_rev(int64_t r0, int64_t r1, const PartTable& pt, F&& f) {
+  int p = pt.P - 1;
+  int64_t t = r1;
+  while (t > r0) {
+    while (p > 0 && pt.off[p] >= t) --p;
+    int64_t start = pt.off[p] > r0 ? pt.off[p] : r0;
+    if (t - start > kSegMax) start = t - kSegMax;
+    f(p, start, t);
+    t = start;
+  }
+}
+
 // ------------------------------------------- packed LDS histograms -------
 // Counters of experts 2m (low half) and 2m+1 (high half) share one 32-bit
 // word at m * kHistStride + bin.  Bins are RAW BF16 bytes; the flush maps them

@@ -3,14 +3,42 @@
 // expert loads f_e (Sec. 2) from stored Top-K indices.
 //
 // Each lane holds 8 experts of a row (one 16-byte load); G = E/8 lanes cover a
-// row and every lane works on U rows per step, so U loads are in flight
-// before any arithmetic.  Counts go to packed LDS histograms indexed by the
-// raw BF16 byte; the flush maps them to kappa bins.
+// row and every lane works on U rows per step; the next step's U loads are
+// issued before a step is counted.  Margins are rounded to BF16 two at a time
+// by the hardware conversion (round to nearest even, subnormals kept).  Counts
+// go to packed LDS histograms indexed by the raw BF16 byte; the flush maps
+// them to kappa bins.
 #include "eqb_internal.hpp"
 
 namespace eqb {
 
 constexpr int kMarginU = 4;   // rows per lane per block step
+
+// Counts the margins of one row piece: eight experts e0 .. e0+7 (four packed
+// BF16 pairs in w) against tau.  Two margins are rounded by one conversion;
+// p holds bf16(tau - z_j) in bits 0..15 and bf16(tau - z_{j+1}) in bits 16..31.
+//  coarse: the raw high bytes are bits 8..15 and 24..31 of p;
+//  fine  : x = p ^ C with C = U_{j+1} << 24 | U_j << 8 (U = raw form of the
+//          selected bin u_e) has zero high bytes exactly for the margins in the
+//          selected bins, and its bits 0..7 / 16..23 are their raw low bytes.
+template <bool kFine>
+__device__ __forceinline__ void count_piece(uint32_t* sh, const uint4& w, float tv, uint32_t row0,
+                                            const uint32_t (&csel)[4]) {
+  const uint32_t w4[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const uint32_t p = bf16x2_bits(tv - bf16_lo(w4[i]), tv - bf16_hi(w4[i]));
+    uint32_t* rowp = sh + row0 + i * kHistStride;
+    if (!kFine) {
+      atomicAdd(rowp + ((p >> 8) & 0xFFu), 1u);
+      atomicAdd(rowp + (p >> 24), 1u << 16);
+    } else {
+      const uint32_t x = p ^ csel[i];
+      if ((x & 0xFF00u) == 0u) atomicAdd(rowp + (x & 0xFFu), 1u);
+      if (x < (1u << 24)) atomicAdd(rowp + ((x >> 16) & 0xFFu), 1u << 16);
+    }
+  }
+}
 
 template <int E, bool kFine>
 __global__ __launch_bounds__(kBlock) void margin_hist_kernel(
@@ -25,54 +53,57 @@ __global__ __launch_bounds__(kBlock) void margin_hist_kernel(
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int g = lane % G, rr = lane / G;
   const int e0 = g * 8;
-  // Fine pass: a margin is counted when the high byte of its rounded BF16
-  // pattern equals the raw form U of u_e.  With y = bits + lsb + (0x7FFF - (U << 24)),
-  // that holds exactly when y < 2^24 (unsigned), and bits 16..23 of y are then
-  // the raw low byte of the rounded pattern.
-  uint32_t cfine[8];
+  const uint32_t row0 = hist_row(e0);
+  uint32_t csel[4];
 #pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    int u = kFine ? sel_hi[e0 + j] : 0;
-    u = (u >= 0 && u < kNBins) ? u : 0;   // invalid selections are skipped at the flush
-    cfine[j] = 0x7FFFu - ((uint32_t)raw_hi_of_kappa(u) << 24);
+  for (int i = 0; i < 4; ++i) {
+    uint32_t c = 0;
+    if (kFine) {
+      int u0 = sel_hi[e0 + 2 * i], u1 = sel_hi[e0 + 2 * i + 1];
+      u0 = (u0 >= 0 && u0 < kNBins) ? u0 : 0;   // invalid selections are skipped at the flush
+      u1 = (u1 >= 0 && u1 < kNBins) ? u1 : 0;
+      c = ((uint32_t)raw_hi_of_kappa(u1) << 24) | ((uint32_t)raw_hi_of_kappa(u0) << 8);
+    }
+    csel[i] = c;
   }
   for (int w = threadIdx.x; w < hist_words<E>(); w += kBlock) sh_hist[w] = 0;
   __syncthreads();
 
   int64_t r0, r1;
   block_rows(T, rows_per_block, &r0, &r1);
-  for_each_segment(r0, r1, pt, [&](int p, int64_t s0, int64_t s1) {
-    for (int64_t base = s0; base < s1; base += ROWS) {
-      uint4 v[kMarginU];
-      float tv[kMarginU];
-      bool ok[kMarginU];
+  // Rows are visited last to first: the route sweep that precedes this one
+  // reads every block range first to last, so the rows it read last may still
+  // be held by the memory-side cache.
+  for_each_segment_rev(r0, r1, pt, [&](int p, int64_t s0, int64_t s1) {
+    uint4 va[kMarginU], vb[kMarginU];
+    float ta[kMarginU], tb[kMarginU];
+    // rows of a step: u * kWaves * R + wave * R + rr; invalid rows read nothing
+    auto load_step = [&](uint4 (&v)[kMarginU], float (&tv)[kMarginU], int64_t base) {
 #pragma unroll
       for (int u = 0; u < kMarginU; ++u) {
         const int64_t t = base + (int64_t)(u * kWaves + wave) * R + rr;
-        ok[u] = t < s1;
         v[u] = make_uint4(0, 0, 0, 0);
         tv[u] = 0.0f;
-        if (ok[u]) {
+        if (t < s1) {
           v[u] = *reinterpret_cast<const uint4*>(z + t * E + e0);
           tv[u] = tau[t];
         }
       }
+    };
+    // the next step's rows are in flight while a step is counted
+    const int64_t last = s0 + ((s1 - 1 - s0) / ROWS) * ROWS;
+    load_step(va, ta, last);
+    for (int64_t base = last; base >= s0; base -= ROWS) {
+      if (base - ROWS >= s0) load_step(vb, tb, base - ROWS);
 #pragma unroll
       for (int u = 0; u < kMarginU; ++u) {
-        if (!ok[u]) continue;
-        const uint32_t w4[4] = {v[u].x, v[u].y, v[u].z, v[u].w};
+        const int64_t t = base + (int64_t)(u * kWaves + wave) * R + rr;
+        if (t < s1) count_piece<kFine>(sh_hist, va[u], ta[u], row0, csel);
+      }
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          const float zf = (j & 1) ? bf16_hi(w4[j >> 1]) : bf16_lo(w4[j >> 1]);
-          const uint32_t bits = __float_as_uint(tv[u] - zf);
-          const uint32_t row = hist_row(e0 + j);
-          if (!kFine) {
-            atomicAdd(&sh_hist[row + bf16_raw_hi(bits)], hist_inc(j));
-          } else {
-            const uint32_t y = bits + ((bits >> 16) & 1u) + cfine[j];
-            if (y < (1u << 24)) atomicAdd(&sh_hist[row + ((y >> 16) & 0xFFu)], hist_inc(j));
-          }
-        }
+      for (int u = 0; u < kMarginU; ++u) {
+        va[u] = vb[u];
+        ta[u] = tb[u];
       }
     }
     __syncthreads();
