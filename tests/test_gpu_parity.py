@@ -238,3 +238,51 @@ def test_bf16_rounding_of_every_high_half_through_both_passes(eqb):
         torch.cuda.synchronize()
         want = O.count_low(keys[:, :2], np.array([u, u]), [0, T])[0]
         np.testing.assert_array_equal(L.cpu().numpy()[0, :2], want, err_msg=f"u={u}")
+
+
+def test_device_rounding_exhaustive_through_both_passes(eqb):
+    """Every finite float32 value tau (2^32 minus Inf/NaN) is a margin tau - 0;
+    its coarse count and its fine count inside every populated coarse bin must
+    equal the oracle's, chunk by chunk (2^24 consecutive patterns per chunk).
+    Counts aggregate, so one rounding error would need another that cancels it
+    in the same bin of the same chunk to go unseen."""
+    from concurrent.futures import ThreadPoolExecutor
+    E, Tc = 8, 1 << 24
+
+    def n_finite(c):
+        return Tc // 2 if (c & 0x7F) == 0x7F else Tc      # exponent 0xFF above the midpoint
+
+    def expected(c):
+        bits = np.arange(c << 24, (c << 24) + n_finite(c), dtype=np.uint64).astype(np.uint32)
+        keys = O.kappa(O.f32_to_bf16_rne(bits.view(np.float32)))
+        hi = (keys >> 8).astype(np.int64)
+        coarse = np.bincount(hi, minlength=256)
+        fine = {int(u): np.bincount((keys[hi == u] & 0xFF).astype(np.int64), minlength=256)
+                for u in np.flatnonzero(coarse)}
+        return coarse, fine
+
+    z = torch.zeros((Tc, E), dtype=torch.int16, device="cuda")
+    H = torch.zeros((1, E, 256), dtype=torch.int32, device="cuda")
+    L = torch.zeros((1, E, 256), dtype=torch.int32, device="cuda")
+    with ThreadPoolExecutor(_threads()) as ex:
+        for c, (coarse, fine) in zip(range(256), ex.map(expected, range(256))):
+            if c % 32 == 0:
+                say(f"device rounding chunk {c:#04x}")
+            n = n_finite(c)
+            start = (c << 24) - (1 << 32 if c >= 0x80 else 0)
+            tau = torch.arange(start, start + n, dtype=torch.int32, device="cuda").view(torch.float32)
+            zc = z[:n]
+            H.zero_()
+            eqb.eqb_margin_hist_pass1(zc, tau, H)
+            got = H.cpu().numpy()[0]
+            for e in range(E):
+                np.testing.assert_array_equal(got[e], coarse, err_msg=f"coarse chunk {c:#x}")
+            us = sorted(fine)
+            for i in range(0, len(us), E):
+                group = us[i:i + E]
+                sel = torch.tensor(group + [group[0]] * (E - len(group)), dtype=torch.int32, device="cuda")
+                L.zero_()
+                eqb.eqb_margin_hist_pass2(zc, tau, sel, L)
+                got = L.cpu().numpy()[0]
+                for j, u in enumerate(group):
+                    np.testing.assert_array_equal(got[j], fine[u], err_msg=f"fine chunk {c:#x} u={u:#x}")

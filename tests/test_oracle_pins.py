@@ -52,6 +52,32 @@ def test_bf16_rounding_matches_torch_on_every_high_half():
         assert np.array_equal(O.f32_to_bf16_rne(x), torch_bf16(x)), hex(low or 0)
 
 
+def test_bf16_rounding_exhaustive_against_torch():
+    """Every finite float32 pattern (2^32 minus Inf/NaN), in chunks of 2^20:
+    the oracle's nearest-neighbour rounding equals torch's conversion."""
+    from concurrent.futures import ThreadPoolExecutor
+
+    def chunk(c):
+        s = c << 20
+        bits = np.arange(s, s + (1 << 20), dtype=np.uint64).astype(np.uint32)
+        bits = bits[(bits & 0x7F800000) != 0x7F800000]
+        if bits.size == 0:
+            return -1
+        x = bits.view(np.float32)
+        bad = np.flatnonzero(O.f32_to_bf16_rne(x) != torch_bf16(x))
+        return int(bits[bad[0]]) if bad.size else -1
+
+    threads = max(1, min(8, os.cpu_count() or 1))
+    torch_threads = torch.get_num_threads()
+    torch.set_num_threads(1)
+    try:
+        with ThreadPoolExecutor(threads) as ex:
+            first_bad = [b for b in ex.map(chunk, range(1 << 12)) if b >= 0]
+    finally:
+        torch.set_num_threads(torch_threads)
+    assert not first_bad, f"rounding differs at {first_bad[0]:#010x}"
+
+
 def test_bf16_rounding_random_patterns():
     rng = np.random.default_rng(11)
     bits = rng.integers(0, 1 << 32, size=1 << 21, dtype=np.uint64).astype(np.uint32)
