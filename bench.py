@@ -92,6 +92,27 @@ def cpu_baseline(w, rows, threads=1):
                       f"{dt:.1f} s on {threads} thread(s) of {os.cpu_count()} visible cores ({cpu_model()})"}
 
 
+def qb_loop_leg(w, eqb, torch, steps, dev, part_off):
+    """The closed QB loop (Eq. 2) over fresh batches of the same distribution,
+    starting from b = 0: Global and Local MaxVio (Sec. 5) of every step."""
+    import workloads as W
+    zs = []
+    for q in range(1, steps + 1):
+        z, _, _ = W.generate(w, batch=q)
+        zs.append(torch.from_numpy(z.view(np.int16)).to(dev))
+        del z
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    res = eqb.qb_loop(zs, torch.zeros(w.E, dtype=torch.float32), w.K, part_off)
+    dt = time.perf_counter() - t0
+    del zs
+    return {"batches": f"fresh draws 1..{steps} of {w.name} (same per-expert offsets), b^(0) = 0",
+            "maxvio_global": [r["maxvio_global"] for r in res],
+            "maxvio_local_max": [float(np.nanmax(r["maxvio_local"])) for r in res],
+            "ms_per_step_wall": dt * 1e3 / steps,
+            "dev_status": max(r["dev_status"] for r in res)}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -100,6 +121,8 @@ def main():
     ap.add_argument("--workload", default="large256")
     ap.add_argument("--cpu-rows", type=int, default=1048576,
                     help="tokens in the CPU-oracle baseline slice (0 disables it)")
+    ap.add_argument("--qb-steps", type=int, default=4,
+                    help="steps of the closed QB loop over fresh batches (0 disables it)")
     ap.add_argument("--stages", action="store_true", help="also print per-stage times to stderr")
     ap.add_argument("--print-source-hash", action="store_true", help="print the kernel source hash and exit")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
@@ -204,6 +227,9 @@ def main():
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": route_gbs / HBM_PEAK_GBS,
                      "traffic": traffic, "algorithmic_bytes": route_bytes},
     }
+    if args.qb_steps > 0:
+        del zt
+        out["qb_loop"] = qb_loop_leg(w, eqb, torch, args.qb_steps, dev, part_off)
     if args.cpu_rows > 0:
         out["cpu_baseline"] = cpu_baseline(w, args.cpu_rows)
     else:

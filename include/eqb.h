@@ -130,6 +130,22 @@ eqb_status eqb_margin_hist_pass2(const uint16_t* z, const float* tau, int64_t T,
 eqb_status eqb_expert_load(const int32_t* topk_idx, int64_t T, int32_t K, int32_t E,
                            const int64_t* part_off, int32_t P, int32_t* load, void* stream);
 
+/*
+ * Balance metric (Sec. 5; Appendix E, "Balance metrics"):
+ *   MaxVio(B) = max_e [ f_e(B) / fbar(B) - 1 ],  fbar(B) = K|B|/E  (Sec. 2).
+ *   load [P,E] int32 (in): per-partition loads f_{p,e}, e.g. from eqb_route_topk.
+ *   maxvio_global [1] binary64 (out): the whole batch, f_e = sum_p f_{p,e}, |B| = T
+ *     ("Global MaxVio").
+ *   maxvio_local [P] binary64 (out, nullable): partition p alone,
+ *     |B| = part_off[p+1] - part_off[p] ("Local MaxVio"); NaN for an empty partition.
+ * Each value is (max_e f_e) * E / (K * |B|) - 1 in binary64: an exact integer
+ * maximum, then one division and one subtraction, each rounded to nearest even.
+ * T = 0 returns EQB_OK and writes nothing.
+ */
+eqb_status eqb_max_violation(const int32_t* load, int64_t T, int32_t K, int32_t E,
+                             const int64_t* part_off, int32_t P, double* maxvio_global,
+                             double* maxvio_local, void* stream);
+
 /* Host helper: r = ceil(T*K/E) (Sec. 3; the paper assumes T*K/E is an
  * integer), or -1 for invalid arguments.  Host only, no HIP call. */
 int64_t eqb_rank(int64_t T_total, int32_t K, int32_t E);

@@ -128,6 +128,20 @@ eqb_status eqb_expert_load(const int32_t* topk_idx, int64_t T, int32_t K, int32_
   return launch_load(topk_idx, T, K, E, load, pt, static_cast<hipStream_t>(stream));
 }
 
+eqb_status eqb_max_violation(const int32_t* load, int64_t T, int32_t K, int32_t E,
+                             const int64_t* part_off, int32_t P, double* maxvio_global,
+                             double* maxvio_local, void* stream) {
+  if (T < 0 || T > INT32_MAX || K < 1 || K >= E) return EQB_ERR_INVALID_ARG;
+  if (!supported_E(E)) return EQB_ERR_UNSUPPORTED;
+  PartTable pt;
+  const eqb_status st = make_table(part_off, P, T, &pt);
+  if (st != EQB_OK) return st;
+  if (T == 0) return EQB_OK;
+  if (!load || !maxvio_global) return EQB_ERR_INVALID_ARG;
+  return launch_max_violation(load, E, K, pt, maxvio_global, maxvio_local,
+                              static_cast<hipStream_t>(stream));
+}
+
 int64_t eqb_rank(int64_t T_total, int32_t K, int32_t E) {
   if (T_total < 0 || E < 1 || K < 1 || K >= E) return -1;
   if (T_total > ((int64_t)1 << 40)) return -1;

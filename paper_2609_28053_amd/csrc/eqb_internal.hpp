@@ -36,6 +36,9 @@ eqb_status launch_select(int pass, const int32_t* hist, int P, int E, int64_t r,
                          int64_t* rank_in_bin, int32_t* sel_lo, uint16_t* q_bf16, float* b_next,
                          int32_t* hist_sum, int32_t* status, hipStream_t s);
 
+eqb_status launch_max_violation(const int32_t* load, int E, int K, const PartTable& pt,
+                                double* out_global, double* out_local, hipStream_t s);
+
 // Number of compute units of the current device (cached per device).
 int num_cus();
 

@@ -8,6 +8,7 @@ missing or unloadable library raises ImportError: there is no fallback.
 """
 from __future__ import annotations
 
+import contextlib
 import ctypes
 import os
 from typing import Optional, Sequence
@@ -33,6 +34,7 @@ EXPORTS = (
     "eqb_select_quantile",
     "eqb_margin_hist_pass2",
     "eqb_expert_load",
+    "eqb_max_violation",
     "eqb_rank",
     "eqb_status_string",
 )
@@ -53,6 +55,7 @@ def _load():
         "eqb_select_quantile": [i32, P, i32, i32, i64, P, P, P, P, P, P, P, P],
         "eqb_margin_hist_pass2": [P, P, i64, i32, P, P, i32, P, P],
         "eqb_expert_load": [P, i64, i32, i32, P, i32, P, P],
+        "eqb_max_violation": [P, i64, i32, i32, P, i32, P, P, P],
         "eqb_rank": [i64, i32, i32],
         "eqb_status_string": [i32],
     }
@@ -165,6 +168,18 @@ def eqb_expert_load(topk_idx, E, load, part_off=None, stream=None):
     del keep
 
 
+def eqb_max_violation(load, T, K, maxvio_global, maxvio_local=None, part_off=None, stream=None):
+    P, E = load.shape
+    po, Pn, keep = _offsets(part_off, T)
+    if Pn != P:
+        raise ValueError(f"load has {P} partitions, part_off describes {Pn}")
+    _check("eqb_max_violation", lib.eqb_max_violation(
+        _ptr(load, torch.int32, P * E, "load"), T, K, E, po, P,
+        _ptr(maxvio_global, torch.float64, 1, "maxvio_global"),
+        _ptr(maxvio_local, torch.float64, P, "maxvio_local"), _stream(stream)))
+    del keep
+
+
 def eqb_rank(T_total: int, K: int, E: int) -> int:
     return int(lib.eqb_rank(T_total, K, E))
 
@@ -230,3 +245,37 @@ def run_layer(z: torch.Tensor, b: torch.Tensor, K: int, part_off=None, fused=Tru
     T, E = z.shape
     P = 1 if part_off is None else len(part_off) - 1
     return Layer(T, E, K, P, device=z.device).run(z, b, part_off, fused, stream)
+
+
+def qb_loop(batches, b0, K: int, part_off=None, stream=None):
+    """The closed QB loop (Eq. 2) on the GPU: batch q is routed with b^(q),
+    its EQB statistics give b^(q+1), which routes batch q+1.  The bias never
+    leaves the device between steps.  Returns one dict per step with host
+    copies of the bias used (b), the loads [P,E], Global and Local MaxVio
+    (Sec. 5) of that routing, b_hat (BF16 bits) and the next bias.  Work is
+    enqueued on ``stream`` (default: the current stream)."""
+    batches = list(batches)
+    if not batches:
+        return []
+    T, E = batches[0].shape
+    P = 1 if part_off is None else len(part_off) - 1
+    dev = batches[0].device
+    ctx = torch.cuda.stream(stream) if stream is not None else contextlib.nullcontext()
+    steps = []
+    with ctx:
+        lay = Layer(T, E, K, P, device=dev)
+        mv_g = torch.empty(1, dtype=torch.float64, device=dev)
+        mv_l = torch.empty(P, dtype=torch.float64, device=dev)
+        b = b0.detach().to(device=dev, dtype=torch.float32).clone()
+        for z in batches:
+            if tuple(z.shape) != (T, E):
+                raise ValueError("every batch of the loop has the same shape")
+            lay.run(z, b, part_off)
+            eqb_max_violation(lay.load, T, K, mv_g, mv_l, part_off)
+            b_used = b.clone()
+            b.copy_(lay.b_next)
+            steps.append(dict(b=b_used.cpu().numpy(), load=lay.load.cpu().numpy(),
+                              maxvio_global=float(mv_g.item()), maxvio_local=mv_l.cpu().numpy(),
+                              bhat=lay.q_bf16.cpu().numpy().view(np.uint16), b_next=b.cpu().numpy(),
+                              dev_status=int(lay.dev_status.item())))
+    return steps

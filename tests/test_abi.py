@@ -30,6 +30,7 @@ def lib():
     lib.eqb_margin_hist_pass2.argtypes = [V, V, i64, i32, V, V, i32, V, V]
     lib.eqb_select_quantile.argtypes = [i32, V, i32, i32, i64, V, V, V, V, V, V, V, V]
     lib.eqb_expert_load.argtypes = [V, i64, i32, i32, V, i32, V, V]
+    lib.eqb_max_violation.argtypes = [V, i64, i32, i32, V, i32, V, V, V]
     lib.eqb_rank.argtypes = [i64, i32, i32]
     lib.eqb_rank.restype = i64
     lib.eqb_status_string.argtypes = [i32]
@@ -121,6 +122,18 @@ def test_select_checks(lib):
     assert s(1, FAKE, 1, 8, 0, FAKE, FAKE, None, None, None, None, None, None) == RANK
     assert s(1, None, 1, 8, 5, FAKE, FAKE, None, None, None, None, None, None) == INVALID
     assert s(2, FAKE, 1, 8, 5, FAKE, FAKE, None, FAKE, None, None, None, None) == INVALID  # no sel_lo
+
+
+def test_max_violation_checks(lib):
+    m = lib.eqb_max_violation
+    assert m(FAKE, 64, 0, 8, None, 1, FAKE, None, None) == INVALID        # K < 1
+    assert m(FAKE, 64, 8, 8, None, 1, FAKE, None, None) == INVALID        # K >= E
+    assert m(FAKE, 64, 2, 12, None, 1, FAKE, None, None) == UNSUPPORTED
+    assert m(None, 64, 2, 8, None, 1, FAKE, None, None) == INVALID
+    assert m(FAKE, 64, 2, 8, None, 1, None, None, None) == INVALID        # no global output
+    po, keep = offs(0, 10, 5, 64)
+    assert m(FAKE, 64, 2, 8, po, 3, FAKE, FAKE, None) == INVALID          # decreasing offsets
+    assert m(FAKE, 0, 2, 8, None, 1, FAKE, None, None) == OK              # empty batch
 
 
 def test_rank_and_status_strings(lib):

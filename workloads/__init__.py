@@ -16,6 +16,9 @@ Every array is produced deterministically from (config, seed):
   * the logits are drawn in row chunks of 2**18 tokens, chunk c using its own
     generator ``default_rng([seed, c])``, so chunks can be produced in any
     order or in parallel threads and the result does not change;
+  * further batches of the same distribution (same offsets, bias and
+    partitions; fresh logits) use ``default_rng([seed, batch, c])`` for
+    batch >= 1, so batch 0 is the workload itself;
   * float32 values are rounded to BF16 by torch's CPU conversion
     (round-to-nearest-even), a library routine independent of both the
     oracle and the kernels.
@@ -95,8 +98,8 @@ def partition_offsets(w: Workload, rng: np.random.Generator) -> np.ndarray:
     return off
 
 
-def _z_chunk(w: Workload, c: int, rows: int, off: np.ndarray) -> np.ndarray:
-    g = np.random.default_rng([w.seed, c])
+def _z_chunk(w: Workload, c: int, rows: int, off: np.ndarray, batch: int = 0) -> np.ndarray:
+    g = np.random.default_rng([w.seed, c] if batch == 0 else [w.seed, batch, c])
     if w.kind == "tie":
         k = g.integers(-TIE_GRID_STEPS, TIE_GRID_STEPS + 1, size=(rows, w.E))
         neg = g.integers(0, 2, size=(rows, w.E)).astype(bool)
@@ -116,8 +119,13 @@ def _z_chunk(w: Workload, c: int, rows: int, off: np.ndarray) -> np.ndarray:
     return _to_bf16_bits(x)
 
 
-def generate(w: Workload, threads: Optional[int] = None):
-    """Return (z_bits uint16 [T,E], b float32 [E], part_off int64 [P+1])."""
+def generate(w: Workload, threads: Optional[int] = None, batch: int = 0):
+    """Return (z_bits uint16 [T,E], b float32 [E], part_off int64 [P+1]).
+
+    ``batch`` selects a fresh draw of the logits from the same distribution;
+    b and part_off do not depend on it."""
+    if batch < 0:
+        raise ValueError("batch must be non-negative")
     rng = np.random.default_rng(w.seed)
     off = (rng.standard_normal(w.E, dtype=np.float32) * np.float32(w.off_sigma)
            if w.off_sigma else np.zeros(w.E, np.float32))
@@ -135,7 +143,7 @@ def generate(w: Workload, threads: Optional[int] = None):
     def work(c):
         r0 = c * CHUNK_ROWS
         r1 = min(w.T, r0 + CHUNK_ROWS)
-        z[r0:r1] = _z_chunk(w, c, r1 - r0, off)
+        z[r0:r1] = _z_chunk(w, c, r1 - r0, off, batch)
 
     n = threads or min(16, os.cpu_count() or 1)
     if nchunks <= 1 or n <= 1:
