@@ -113,6 +113,34 @@ def qb_loop_leg(w, eqb, torch, steps, dev, part_off):
             "dev_status": max(r["dev_status"] for r in res)}
 
 
+def lei_leg(w, eqb, torch, lay, part_off, stream, reps=10):
+    """Load-Error Injection (Sec. 4) after the step: the residual from the
+    step's per-partition loads and the injection into a [T,E] binary32
+    score-gradient buffer (read and written once: 8 bytes per score)."""
+    dev = lay.load.device
+    inj = torch.empty((w.P, w.E), dtype=torch.float32, device=dev)
+    grad = torch.zeros((w.T, w.E), dtype=torch.float32, device=dev)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+    with torch.cuda.stream(stream):
+        for _ in range(2):
+            eqb.eqb_lei_residual(lay.load, w.T, w.K, 2e-5, 1.0, inj, part_off, stream)
+            eqb.eqb_lei_inject(grad, inj, part_off, stream)
+        ev[0].record(stream)
+        for _ in range(reps):
+            eqb.eqb_lei_residual(lay.load, w.T, w.K, 2e-5, 1.0, inj, part_off, stream)
+        ev[1].record(stream)
+        for _ in range(reps):
+            eqb.eqb_lei_inject(grad, inj, part_off, stream)
+        ev[2].record(stream)
+    torch.cuda.synchronize()
+    inject_ms = ev[1].elapsed_time(ev[2]) / reps
+    gbs = 8.0 * w.T * w.E / (inject_ms * 1e-3) / 1e9
+    del grad
+    return {"residual_us": ev[0].elapsed_time(ev[1]) * 1e3 / reps, "inject_ms": inject_ms,
+            "inject_bytes": 8 * w.T * w.E, "inject_gbs": gbs, "inject_frac_of_peak": gbs / HBM_PEAK_GBS,
+            "eta": 2e-5, "c": 1.0}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -227,6 +255,7 @@ def main():
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": route_gbs / HBM_PEAK_GBS,
                      "traffic": traffic, "algorithmic_bytes": route_bytes},
     }
+    out["lei"] = lei_leg(w, eqb, torch, lay, part_off, stream)
     if args.qb_steps > 0:
         del zt
         out["qb_loop"] = qb_loop_leg(w, eqb, torch, args.qb_steps, dev, part_off)

@@ -146,6 +146,32 @@ eqb_status eqb_max_violation(const int32_t* load, int64_t T, int32_t K, int32_t 
                              const int64_t* part_off, int32_t P, double* maxvio_global,
                              double* maxvio_local, void* stream);
 
+/*
+ * Load-Error Injection, the residual (Sec. 4, Eq. lei and the normalisation
+ * that bounds it).  For each partition p (a local batch B_l):
+ *   rho_{p,e} = f_{p,e} / fbar(B_p) - 1 = f_{p,e} E / (K |B_p|) - 1,
+ *   with c > 0: xi_p = max_e |rho_{p,e}| / c and rho~ = rho * tanh(xi_p)/xi_p
+ *   (tanh(xi)/xi := 1 at xi = 0); with c <= 0: rho~ = rho (unnormalised LEI);
+ *   inj[p,e] = eta * rho~_{p,e}, computed in binary64, rounded once to binary32.
+ *   load [P,E] int32 (in); inj [P,E] binary32 (out, 16-byte aligned for
+ *   eqb_lei_inject).  An empty partition gets inj = 0.  Unlike the other calls,
+ *   T = 0 still writes inj (all zero).  NaN eta or c is EQB_ERR_INVALID_ARG.
+ */
+eqb_status eqb_lei_residual(const int32_t* load, int64_t T, int32_t K, int32_t E,
+                            const int64_t* part_off, int32_t P, double eta, double c, float* inj,
+                            void* stream);
+
+/*
+ * Load-Error Injection, the gradient correction (Sec. 4, Eq. lei):
+ *   grad_s[t,e] += inj[p,e] for every token t of partition p, one binary32
+ *   addition each (round to nearest even).  LEI leaves routing and mixture
+ *   weights unchanged; only the router-score gradient moves.
+ *   grad_s [T,E] binary32 (in/out, 16-byte aligned); inj [P,E] binary32 (in,
+ *   16-byte aligned), e.g. from eqb_lei_residual.
+ */
+eqb_status eqb_lei_inject(float* grad_s, const float* inj, int64_t T, int32_t E,
+                          const int64_t* part_off, int32_t P, void* stream);
+
 /* Host helper: r = ceil(T*K/E) (Sec. 3; the paper assumes T*K/E is an
  * integer), or -1 for invalid arguments.  Host only, no HIP call. */
 int64_t eqb_rank(int64_t T_total, int32_t K, int32_t E);

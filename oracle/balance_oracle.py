@@ -13,6 +13,11 @@ Written from arXiv 2609.28053:
   batch, Local MaxVio those of one local batch (a partition here).
 * The closed QB loop (Eq. 2): the statistics of step q give the bias
   b^(q+1) that routes the batch of step q+1.
+* Load-Error Injection (Sec. 4, Eq. lei and the normalisation that bounds
+  it): for a local batch, rho_e = f_e/fbar - 1 = E (F_e - Q_e); optionally
+  rho~ = rho tanh(xi)/xi with xi = ||rho||_inf / c (and tanh(xi)/xi := 1 at
+  xi = 0); the router-score gradient of every token of that local batch gets
+  grad_{s_{t,e}} += eta rho~_e.
 
 Readings taken where the paper is silent:
   * MaxVio is evaluated in binary64 as (max_e f_e) * E / (K |B|) - 1: the
@@ -21,8 +26,16 @@ Readings taken where the paper is silent:
     f_e/fbar - 1 over e is attained at the largest f_e because the map is
     increasing.)
   * An empty batch has no uniform target; its MaxVio is NaN.
+  * LEI's injected value eta * rho~_e is computed in binary64 as
+    rho = (f E)/(K |B|) - 1, xi = max|rho| / c, rho~ = rho * (tanh(xi)/xi),
+    value = eta * rho~, and rounded once to binary32; c <= 0 means the
+    unnormalised form (rho~ = rho).  An empty local batch injects 0.
+  * The injection itself is one binary32 addition per score, rounded to
+    nearest even.
 """
 from __future__ import annotations
+
+import math
 
 import numpy as np
 
@@ -71,3 +84,38 @@ def qb_loop(batches, b0, K: int, part_off=None, threads: int = 1):
                           bhat=res["bhat"], b_next=res["b_next"]))
         b = res["b_next"].astype(np.float32)
     return steps
+
+
+# --------------------------------------------------------------------------
+# Load-Error Injection (Sec. 4, Eq. lei and its normalisation)
+# --------------------------------------------------------------------------
+def lei_residual(load_pe, part_off, K: int, eta: float, c: float) -> np.ndarray:
+    """The value each partition injects into its router-score gradients,
+    eta * rho~_{p,e}, as binary32 [P,E]."""
+    load_pe = np.asarray(load_pe, dtype=np.int64)
+    part_off = np.asarray(part_off, dtype=np.int64)
+    P, E = load_pe.shape
+    out = np.zeros((P, E), np.float32)
+    for p in range(P):
+        n = int(part_off[p + 1] - part_off[p])
+        if n == 0:
+            continue
+        rho = [float(f * E) / float(K * n) - 1.0 for f in load_pe[p]]
+        scale = 1.0
+        if c > 0:
+            xi = max(abs(v) for v in rho) / float(c)
+            scale = math.tanh(xi) / xi if xi > 0 else 1.0
+        out[p] = np.array([float(eta) * (v * scale) for v in rho], dtype=np.float64).astype(np.float32)
+    return out
+
+
+def lei_inject(grad_s, inj, part_off) -> np.ndarray:
+    """grad_{s_{t,e}} + eta rho~_{p(t),e} for every token t of partition p,
+    one binary32 addition each."""
+    grad_s = np.asarray(grad_s, dtype=np.float32)
+    part_off = np.asarray(part_off, dtype=np.int64)
+    out = grad_s.copy()
+    for p in range(len(part_off) - 1):
+        r0, r1 = int(part_off[p]), int(part_off[p + 1])
+        out[r0:r1] = (grad_s[r0:r1] + inj[p][None, :]).astype(np.float32)
+    return out

@@ -1,5 +1,6 @@
 // balance.hip - load-balance quantities computed from the expert loads:
-// MaxVio (arXiv 2609.28053, Sec. 5 and Appendix E, "Balance metrics").
+// MaxVio (arXiv 2609.28053, Sec. 5 and Appendix E, "Balance metrics") and
+// Load-Error Injection (Sec. 4, Eq. lei and its normalisation).
 #include "eqb_internal.hpp"
 
 namespace eqb {
@@ -44,6 +45,99 @@ __global__ __launch_bounds__(kNBins) void max_violation_kernel(
 eqb_status launch_max_violation(const int32_t* load, int E, int K, const PartTable& pt,
                                 double* out_global, double* out_local, hipStream_t s) {
   max_violation_kernel<<<pt.P + 1, kNBins, 0, s>>>(load, E, K, pt, out_global, out_local);
+  return launch_status();
+}
+
+// ------------------------------------------------- Load-Error Injection --
+// Block p: rho_e = f_{p,e} E / (K |B_p|) - 1 in binary64; with c > 0 the
+// shared scale tanh(xi)/xi, xi = max_e |rho_e| / c (1 at xi = 0); the value
+// injected into every score gradient of partition p is eta * (rho_e * scale),
+// rounded once to binary32.  An empty partition injects 0.
+__global__ __launch_bounds__(kNBins) void lei_residual_kernel(
+    const int32_t* __restrict__ load, int E, int K, const PartTable pt, double eta, double c,
+    float* __restrict__ inj) {
+  __shared__ double sh_max[kNBins / 64];
+  const int p = blockIdx.x;
+  const int e = threadIdx.x;
+  const int64_t n = pt.off[p + 1] - pt.off[p];
+  double rho = 0.0;
+  if (e < E && n > 0) rho = (double)((int64_t)load[(int64_t)p * E + e] * E) / ((double)K * (double)n) - 1.0;
+  double a = fabs(rho);
+  for (int off = 32; off > 0; off >>= 1) a = fmax(a, __shfl_xor(a, off));
+  if ((e & 63) == 0) sh_max[e >> 6] = a;
+  __syncthreads();
+  double m = sh_max[0];
+  for (int w = 1; w < (int)(blockDim.x >> 6); ++w) m = fmax(m, sh_max[w]);
+  double scale = 1.0;
+  if (c > 0.0) {
+    const double xi = m / c;
+    if (xi > 0.0) scale = tanh(xi) / xi;
+  }
+  if (e < E) inj[(int64_t)p * E + e] = n > 0 ? (float)(eta * (rho * scale)) : 0.0f;
+}
+
+// grad_s[t,e] += inj[p(t),e], one binary32 addition per score.  G = E/4
+// lanes cover a row with one 16-byte access each; every lane handles kLeiU
+// rows per step, so that many loads are in flight before the first store.
+constexpr int kLeiU = 4;
+
+template <int E>
+__global__ __launch_bounds__(kBlock) void lei_inject_kernel(
+    float* __restrict__ grad, const float* __restrict__ inj, int64_t T, const PartTable pt,
+    int64_t rows_per_block) {
+  constexpr int G = E / 4;
+  constexpr int R = 64 / G;
+  constexpr int ROWS = kWaves * R * kLeiU;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int g = lane % G, rr = lane / G;
+  int64_t r0, r1;
+  block_rows(T, rows_per_block, &r0, &r1);
+  for_each_segment(r0, r1, pt, [&](int p, int64_t s0, int64_t s1) {
+    const float4 d = *reinterpret_cast<const float4*>(inj + (int64_t)p * E + g * 4);
+    for (int64_t base = s0; base < s1; base += ROWS) {
+      float4 v[kLeiU];
+#pragma unroll
+      for (int u = 0; u < kLeiU; ++u) {
+        const int64_t t = base + (int64_t)(u * kWaves + wave) * R + rr;
+        if (t < s1) v[u] = *reinterpret_cast<const float4*>(grad + t * E + g * 4);
+      }
+#pragma unroll
+      for (int u = 0; u < kLeiU; ++u) {
+        const int64_t t = base + (int64_t)(u * kWaves + wave) * R + rr;
+        if (t < s1) {
+          const float4 o = make_float4(v[u].x + d.x, v[u].y + d.y, v[u].z + d.z, v[u].w + d.w);
+          *reinterpret_cast<float4*>(grad + t * E + g * 4) = o;
+        }
+      }
+    }
+  });
+}
+
+eqb_status launch_lei_residual(const int32_t* load, int E, int K, const PartTable& pt, double eta,
+                               double c, float* inj, hipStream_t s) {
+  lei_residual_kernel<<<pt.P, kNBins, 0, s>>>(load, E, K, pt, eta, c, inj);
+  return launch_status();
+}
+
+template <int E>
+static void launch_inject_e(float* grad, const float* inj, int64_t T, const PartTable& pt, hipStream_t s) {
+  int blocks;
+  int64_t rpb;
+  grid_for(T, kWaves * (64 / (E / 4)) * kLeiU, 2, &blocks, &rpb);
+  lei_inject_kernel<E><<<blocks, kBlock, 0, s>>>(grad, inj, T, pt, rpb);
+}
+
+eqb_status launch_lei_inject(float* grad, const float* inj, int64_t T, int E, const PartTable& pt,
+                             hipStream_t s) {
+  switch (E) {
+    case 8: launch_inject_e<8>(grad, inj, T, pt, s); break;
+    case 16: launch_inject_e<16>(grad, inj, T, pt, s); break;
+    case 32: launch_inject_e<32>(grad, inj, T, pt, s); break;
+    case 64: launch_inject_e<64>(grad, inj, T, pt, s); break;
+    case 128: launch_inject_e<128>(grad, inj, T, pt, s); break;
+    case 256: launch_inject_e<256>(grad, inj, T, pt, s); break;
+    default: return EQB_ERR_UNSUPPORTED;
+  }
   return launch_status();
 }
 

@@ -142,6 +142,32 @@ eqb_status eqb_max_violation(const int32_t* load, int64_t T, int32_t K, int32_t 
                               static_cast<hipStream_t>(stream));
 }
 
+eqb_status eqb_lei_residual(const int32_t* load, int64_t T, int32_t K, int32_t E,
+                            const int64_t* part_off, int32_t P, double eta, double c, float* inj,
+                            void* stream) {
+  if (T < 0 || T > INT32_MAX || K < 1 || K >= E) return EQB_ERR_INVALID_ARG;
+  if (!supported_E(E)) return EQB_ERR_UNSUPPORTED;
+  if (!(eta == eta) || !(c == c)) return EQB_ERR_INVALID_ARG;     // NaN coefficients
+  PartTable pt;
+  const eqb_status st = make_table(part_off, P, T, &pt);
+  if (st != EQB_OK) return st;
+  if (!load || !inj) return EQB_ERR_INVALID_ARG;
+  return launch_lei_residual(load, E, K, pt, eta, c, inj, static_cast<hipStream_t>(stream));
+}
+
+eqb_status eqb_lei_inject(float* grad_s, const float* inj, int64_t T, int32_t E,
+                          const int64_t* part_off, int32_t P, void* stream) {
+  if (T < 0 || T > INT32_MAX) return EQB_ERR_INVALID_ARG;
+  if (!supported_E(E)) return EQB_ERR_UNSUPPORTED;
+  PartTable pt;
+  const eqb_status st = make_table(part_off, P, T, &pt);
+  if (st != EQB_OK) return st;
+  if (T == 0) return EQB_OK;
+  if (!grad_s || !inj) return EQB_ERR_INVALID_ARG;
+  if (!aligned16(grad_s) || !aligned16(inj)) return EQB_ERR_UNSUPPORTED;
+  return launch_lei_inject(grad_s, inj, T, E, pt, static_cast<hipStream_t>(stream));
+}
+
 int64_t eqb_rank(int64_t T_total, int32_t K, int32_t E) {
   if (T_total < 0 || E < 1 || K < 1 || K >= E) return -1;
   if (T_total > ((int64_t)1 << 40)) return -1;

@@ -39,6 +39,11 @@ eqb_status launch_select(int pass, const int32_t* hist, int P, int E, int64_t r,
 eqb_status launch_max_violation(const int32_t* load, int E, int K, const PartTable& pt,
                                 double* out_global, double* out_local, hipStream_t s);
 
+eqb_status launch_lei_residual(const int32_t* load, int E, int K, const PartTable& pt, double eta,
+                               double c, float* inj, hipStream_t s);
+eqb_status launch_lei_inject(float* grad, const float* inj, int64_t T, int E, const PartTable& pt,
+                             hipStream_t s);
+
 // Number of compute units of the current device (cached per device).
 int num_cus();
 

@@ -35,6 +35,8 @@ EXPORTS = (
     "eqb_margin_hist_pass2",
     "eqb_expert_load",
     "eqb_max_violation",
+    "eqb_lei_residual",
+    "eqb_lei_inject",
     "eqb_rank",
     "eqb_status_string",
 )
@@ -56,6 +58,8 @@ def _load():
         "eqb_margin_hist_pass2": [P, P, i64, i32, P, P, i32, P, P],
         "eqb_expert_load": [P, i64, i32, i32, P, i32, P, P],
         "eqb_max_violation": [P, i64, i32, i32, P, i32, P, P, P],
+        "eqb_lei_residual": [P, i64, i32, i32, P, i32, ctypes.c_double, ctypes.c_double, P, P],
+        "eqb_lei_inject": [P, P, i64, i32, P, i32, P],
         "eqb_rank": [i64, i32, i32],
         "eqb_status_string": [i32],
     }
@@ -177,6 +181,26 @@ def eqb_max_violation(load, T, K, maxvio_global, maxvio_local=None, part_off=Non
         _ptr(load, torch.int32, P * E, "load"), T, K, E, po, P,
         _ptr(maxvio_global, torch.float64, 1, "maxvio_global"),
         _ptr(maxvio_local, torch.float64, P, "maxvio_local"), _stream(stream)))
+    del keep
+
+
+def eqb_lei_residual(load, T, K, eta, c, inj, part_off=None, stream=None):
+    P, E = load.shape
+    po, Pn, keep = _offsets(part_off, T)
+    if Pn != P:
+        raise ValueError(f"load has {P} partitions, part_off describes {Pn}")
+    _check("eqb_lei_residual", lib.eqb_lei_residual(
+        _ptr(load, torch.int32, P * E, "load"), T, K, E, po, P, float(eta), float(c),
+        _ptr(inj, torch.float32, P * E, "inj"), _stream(stream)))
+    del keep
+
+
+def eqb_lei_inject(grad_s, inj, part_off=None, stream=None):
+    T, E = grad_s.shape
+    po, P, keep = _offsets(part_off, T)
+    _check("eqb_lei_inject", lib.eqb_lei_inject(
+        _ptr(grad_s, torch.float32, T * E, "grad_s"), _ptr(inj, torch.float32, P * E, "inj"), T, E,
+        po, P, _stream(stream)))
     del keep
 
 

@@ -31,6 +31,8 @@ def lib():
     lib.eqb_select_quantile.argtypes = [i32, V, i32, i32, i64, V, V, V, V, V, V, V, V]
     lib.eqb_expert_load.argtypes = [V, i64, i32, i32, V, i32, V, V]
     lib.eqb_max_violation.argtypes = [V, i64, i32, i32, V, i32, V, V, V]
+    lib.eqb_lei_residual.argtypes = [V, i64, i32, i32, V, i32, ctypes.c_double, ctypes.c_double, V, V]
+    lib.eqb_lei_inject.argtypes = [V, V, i64, i32, V, i32, V]
     lib.eqb_rank.argtypes = [i64, i32, i32]
     lib.eqb_rank.restype = i64
     lib.eqb_status_string.argtypes = [i32]
@@ -134,6 +136,24 @@ def test_max_violation_checks(lib):
     po, keep = offs(0, 10, 5, 64)
     assert m(FAKE, 64, 2, 8, po, 3, FAKE, FAKE, None) == INVALID          # decreasing offsets
     assert m(FAKE, 0, 2, 8, None, 1, FAKE, None, None) == OK              # empty batch
+
+
+def test_lei_checks(lib):
+    r = lib.eqb_lei_residual
+    assert r(FAKE, 64, 2, 8, None, 1, 1e-5, 2.0, None, None) == INVALID     # no output
+    assert r(None, 64, 2, 8, None, 1, 1e-5, 2.0, FAKE, None) == INVALID
+    assert r(FAKE, 64, 8, 8, None, 1, 1e-5, 2.0, FAKE, None) == INVALID     # K >= E
+    assert r(FAKE, 64, 2, 24, None, 1, 1e-5, 2.0, FAKE, None) == UNSUPPORTED
+    assert r(FAKE, 64, 2, 8, None, 1, float("nan"), 2.0, FAKE, None) == INVALID
+    assert r(FAKE, 64, 2, 8, None, 1, 1e-5, float("nan"), FAKE, None) == INVALID
+    i = lib.eqb_lei_inject
+    assert i(None, FAKE, 64, 8, None, 1, None) == INVALID
+    assert i(FAKE, None, 64, 8, None, 1, None) == INVALID
+    assert i(ctypes.c_void_p(0x10004), FAKE, 64, 8, None, 1, None) == UNSUPPORTED   # misaligned
+    assert i(FAKE, FAKE, 64, 12, None, 1, None) == UNSUPPORTED
+    po, keep = offs(0, 10, 63)
+    assert i(FAKE, FAKE, 64, 8, po, 2, None) == INVALID
+    assert i(FAKE, FAKE, 0, 8, None, 1, None) == OK
 
 
 def test_rank_and_status_strings(lib):

@@ -74,3 +74,75 @@ def test_qb_loop_matches_oracle(eqb, name, T, P, steps):
     zs = [torch.from_numpy(z.view(np.int16)).cuda() for z in batches]
     got = eqb.qb_loop(zs, torch.from_numpy(b0), w.K, [int(x) for x in off])
     check_loop(got, want)
+
+
+# ------------------------------------------------------ Load-Error Injection --
+def ulp32(x):
+    x = np.abs(np.asarray(x, np.float32))
+    return np.spacing(x).astype(np.float64)
+
+
+@pytest.mark.parametrize("E,P,c", [(8, 1, 0.0), (64, 4, 2.0), (256, 16, 2.0), (256, 16, 0.0),
+                                   (128, 256, 0.5)])
+def test_lei_residual_matches_oracle(eqb, E, P, c):
+    rng = np.random.default_rng(E + P)
+    K = max(1, E // 32)
+    sizes = rng.integers(0, 4000, size=P)
+    if P > 1:
+        sizes[P // 2] = 0
+    off = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int64)
+    T = int(off[-1])
+    w = rng.dirichlet(np.ones(E) * 0.4)
+    load = np.stack([rng.multinomial(int(K * n), w) for n in sizes]).astype(np.int32)
+    eta = 3.0e-5
+    say(f"lei residual E={E} P={P} c={c}")
+    inj = torch.empty((P, E), dtype=torch.float32, device="cuda")
+    eqb.eqb_lei_residual(torch.from_numpy(load).cuda(), T, K, eta, c, inj, [int(x) for x in off])
+    got = inj.cpu().numpy()
+    want = B.lei_residual(load, off, K, eta, c)
+    if c <= 0:
+        np.testing.assert_array_equal(got.view(np.uint32), want.view(np.uint32))
+    else:
+        # tanh may differ in its last binary64 bit between the device and the
+        # host library; after one rounding to binary32 that is at most one ulp
+        assert np.all(np.abs(got.astype(np.float64) - want) <= ulp32(want))
+
+
+@pytest.mark.parametrize("E,T,P", [(8, 1001, 1), (64, 20011, 5), (256, 70001, 16), (128, 333, 256)])
+def test_lei_inject_matches_oracle(eqb, E, T, P):
+    rng = np.random.default_rng(T)
+    if P >= T:
+        off = np.linspace(0, T, P + 1).astype(np.int64)
+    else:
+        off = np.concatenate([[0], np.sort(rng.choice(np.arange(1, T), P - 1, replace=False)), [T]])
+    if P > 2:
+        off[2] = off[1]                                     # an empty partition
+    off = np.maximum.accumulate(off).astype(np.int64)
+    g = rng.standard_normal((T, E)).astype(np.float32)
+    inj = (rng.standard_normal((P, E)) * 1e-3).astype(np.float32)
+    say(f"lei inject E={E} T={T} P={P}")
+    gt = torch.from_numpy(g).cuda()
+    eqb.eqb_lei_inject(gt, torch.from_numpy(inj).cuda(), [int(x) for x in off])
+    want = B.lei_inject(g, inj, off)
+    np.testing.assert_array_equal(gt.cpu().numpy().view(np.uint32), want.view(np.uint32))
+
+
+def test_lei_on_a_routed_layer(eqb):
+    """Loads from the routing kernel feed the residual; the injection moves
+    only the score gradients, by each partition's value."""
+    w = W.CONFIGS["large256"].with_T(65536, 16)
+    z, b, off = W.generate(w)
+    offl = [int(x) for x in off]
+    say("lei on a routed layer")
+    lay = eqb.run_layer(torch.from_numpy(z.view(np.int16)).cuda(), torch.from_numpy(b).cuda(), w.K, offl)
+    inj = torch.empty((w.P, w.E), dtype=torch.float32, device="cuda")
+    eqb.eqb_lei_residual(lay.load, w.T, w.K, 2e-5, 1.0, inj, offl)
+    grad = torch.zeros((w.T, w.E), dtype=torch.float32, device="cuda")
+    eqb.eqb_lei_inject(grad, inj, offl)
+    torch.cuda.synchronize()
+    want_inj = B.lei_residual(lay.load.cpu().numpy(), off, w.K, 2e-5, 1.0)
+    got_inj = inj.cpu().numpy()
+    assert np.all(np.abs(got_inj.astype(np.float64) - want_inj) <= ulp32(want_inj))
+    gg = grad.cpu().numpy()
+    for p in range(w.P):
+        np.testing.assert_array_equal(gg[off[p]:off[p + 1]], np.broadcast_to(got_inj[p], (off[p + 1] - off[p], w.E)))
