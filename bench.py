@@ -141,6 +141,39 @@ def lei_leg(w, eqb, torch, lay, part_off, stream, reps=10):
             "eta": 2e-5, "c": 1.0}
 
 
+def variants_leg(w, eqb, torch, zt, bt, lay, part_off):
+    """The statistics EQB is compared with (Sec. 2), on the same batch: the
+    rank-averaged quantile (P shards, and P/4 shards to show that it depends
+    on the split) and the fixed-resolution histogram estimate (256 bins on
+    [-8, 8)), each against EQB's exact global quantile b_hat."""
+    exact = (lay.q_bf16.to(torch.int32).cpu().numpy().astype(np.uint32) << 16).view(np.float32)
+    exact = exact.astype(np.float64)
+    out = {}
+    t0 = time.perf_counter()
+    ra = eqb.rank_averaged_qb(zt, bt, w.K, part_off)
+    out["rank_avg_ms_wall"] = (time.perf_counter() - t0) * 1e3
+    coarse = [part_off[i] for i in range(0, len(part_off), 4)]
+    if coarse[-1] != part_off[-1]:
+        coarse.append(part_off[-1])
+    ra4 = eqb.rank_averaged_qb(zt, bt, w.K, coarse)
+    t0 = time.perf_counter()
+    hq = eqb.histogram_qb(zt, bt, w.K, -8.0, 8.0, 256, part_off)
+    out["histogram_ms_wall"] = (time.perf_counter() - t0) * 1e3
+    d = lambda a: np.abs(a - exact)
+    out.update({
+        "rank_avg_P": len(part_off) - 1,
+        "rank_avg_max_abs_err": float(d(ra["b_avg"]).max()),
+        "rank_avg_mean_abs_err": float(d(ra["b_avg"]).mean()),
+        "rank_avg_split_dependence_max_abs": float(np.abs(ra["b_avg"] - ra4["b_avg"]).max()),
+        "rank_avg_coarse_P": len(coarse) - 1,
+        "histogram_bins": 256, "histogram_range": [-8.0, 8.0],
+        "histogram_max_abs_err": float(d(hq["est"]).max()),
+        "histogram_mean_abs_err": float(d(hq["est"]).mean()),
+        "dev_status": max(ra["dev_status"], ra4["dev_status"], hq["dev_status"]),
+    })
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -256,6 +289,7 @@ def main():
                      "traffic": traffic, "algorithmic_bytes": route_bytes},
     }
     out["lei"] = lei_leg(w, eqb, torch, lay, part_off, stream)
+    out["variants"] = variants_leg(w, eqb, torch, zt, bt, lay, part_off)
     if args.qb_steps > 0:
         del zt
         out["qb_loop"] = qb_loop_leg(w, eqb, torch, args.qb_steps, dev, part_off)

@@ -131,6 +131,54 @@ eqb_status eqb_expert_load(const int32_t* topk_idx, int64_t T, int32_t K, int32_
                            const int64_t* part_off, int32_t P, int32_t* load, void* stream);
 
 /*
+ * The statistics EQB is compared with (Sec. 2, after Eq. 2; Sec. 3).
+ *
+ * Rank-averaged QB: every shard (partition) takes the K/E quantile of its own
+ * margins and the shards average them.  Each shard's quantile is exact, found
+ * by the two passes of Algorithm 1 run on that shard's counts alone:
+ *   eqb_select_quantile_local(1, hist_hi [P,E,256]) -> sel_hi, rank_in_bin [P,E]
+ *     with r_p = ceil(|B_p| K / E) (no summing over partitions);
+ *   eqb_margin_hist_pass2_local: like eqb_margin_hist_pass2, but partition p
+ *     counts inside its own bin sel_hi[p,e];
+ *   eqb_select_quantile_local(2, hist_lo [P,E,256]) -> sel_lo, q_bf16 [P,E]
+ *     (q_bf16[p,e] = b_hat_{p,e}, shard p's r_p-th smallest BF16 margin);
+ *   eqb_rank_average: b_avg[e] = sum over non-empty p (binary64, ascending p)
+ *     of b_hat_{p,e}, divided by their number (nullable output), and b_next =
+ *     b_avg - mean(b_avg), centred as in Eq. 2.
+ * An empty partition gets sel = -1 and a NaN q_bf16 and is left out of the
+ * average.  dev_status as for eqb_select_quantile.  T and part_off describe
+ * the whole batch as in every other call; K < E.
+ */
+eqb_status eqb_select_quantile_local(int32_t pass, const int32_t* hist, int64_t T, int32_t K, int32_t E,
+                                     const int64_t* part_off, int32_t P, int32_t* sel_hi,
+                                     int64_t* rank_in_bin, int32_t* sel_lo, uint16_t* q_bf16,
+                                     int32_t* dev_status, void* stream);
+eqb_status eqb_margin_hist_pass2_local(const uint16_t* z, const float* tau, int64_t T, int32_t E,
+                                       const int32_t* sel_hi, const int64_t* part_off, int32_t P,
+                                       int32_t* hist_lo, void* stream);
+eqb_status eqb_rank_average(const uint16_t* q_bf16, int64_t T, int32_t E, const int64_t* part_off,
+                            int32_t P, double* b_avg, float* b_next, void* stream);
+
+/*
+ * Fixed-resolution histogram QB: margin counts over nbins uniform bins of
+ * [lo, hi), summed over the shards, and the quantile read off the sum.
+ *   eqb_margin_hist_uniform: hist[p,e,j] += #{t in p : bin(tau_t - z_{t,e}) = j},
+ *     the margin being the binary32 difference (no BF16 rounding) and
+ *     bin(m) = floor((m - lo) * s) clamped to [0, nbins-1], with
+ *     s = nbins / (hi - lo), all in binary32.  hist [P,E,nbins] int32 (+=).
+ *   eqb_select_uniform: sums the P slabs, finds the first bin j whose running
+ *     count C_j reaches r and writes est[e] = lo + (j + (r - C_{j-1}) / H_j) *
+ *     (hi - lo) / nbins in binary64 (linear within the bin), and, if b_next is
+ *     not NULL, b_next = est - mean(est) centred as in Eq. 2.
+ * 1 <= nbins <= 256 and lo < hi (finite) or EQB_ERR_INVALID_ARG.
+ */
+eqb_status eqb_margin_hist_uniform(const uint16_t* z, const float* tau, int64_t T, int32_t E,
+                                   const int64_t* part_off, int32_t P, float lo, float hi, int32_t nbins,
+                                   int32_t* hist, void* stream);
+eqb_status eqb_select_uniform(const int32_t* hist, int32_t P, int32_t E, int32_t nbins, int64_t r, float lo,
+                              float hi, double* est, float* b_next, int32_t* dev_status, void* stream);
+
+/*
  * Balance metric (Sec. 5; Appendix E, "Balance metrics"):
  *   MaxVio(B) = max_e [ f_e(B) / fbar(B) - 1 ],  fbar(B) = K|B|/E  (Sec. 2).
  *   load [P,E] int32 (in): per-partition loads f_{p,e}, e.g. from eqb_route_topk.

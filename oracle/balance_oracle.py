@@ -18,6 +18,11 @@ Written from arXiv 2609.28053:
   rho~ = rho tanh(xi)/xi with xi = ||rho||_inf / c (and tanh(xi)/xi := 1 at
   xi = 0); the router-score gradient of every token of that local batch gets
   grad_{s_{t,e}} += eta rho~_e.
+* The two distributed QB statistics EQB is compared with (Sec. 2, after
+  Eq. 2; Sec. 3): the rank-averaged quantile, where each rank takes the K/E
+  quantile of its own shard and the ranks average them, and the
+  fixed-resolution histogram estimate, where the ranks all-reduce margin
+  counts over fixed bins and read the quantile off the summed histogram.
 
 Readings taken where the paper is silent:
   * MaxVio is evaluated in binary64 as (max_e f_e) * E / (K |B|) - 1: the
@@ -32,6 +37,16 @@ Readings taken where the paper is silent:
     unnormalised form (rho~ = rho).  An empty local batch injects 0.
   * The injection itself is one binary32 addition per score, rounded to
     nearest even.
+  * Rank-averaged QB: shard p's quantile is its exact r_p-th smallest BF16
+    margin, r_p = ceil(|B_p| K/E); the average over the non-empty shards is a
+    binary64 sum in ascending p divided by their number; the result is
+    centred like Eq. 2 (binary64 mean over e, one rounding to binary32).
+  * Fixed-resolution histogram: the margin is the binary32 difference
+    tau - z (no BF16 rounding); with w = hi - lo and s = nbins / w, both
+    binary32, its bin is floor((m - lo) * s) in binary32, clamped to
+    [0, nbins-1].  The r-th smallest is read as lo + (j + (r - C_{j-1}) / H_j)
+    * (hi - lo) / nbins in binary64 (j the first bin whose running count C_j
+    reaches r, linear within the bin), then centred like Eq. 2.
 """
 from __future__ import annotations
 
@@ -119,3 +134,82 @@ def lei_inject(grad_s, inj, part_off) -> np.ndarray:
         r0, r1 = int(part_off[p]), int(part_off[p + 1])
         out[r0:r1] = (grad_s[r0:r1] + inj[p][None, :]).astype(np.float32)
     return out
+
+
+# --------------------------------------------------------------------------
+# The statistics EQB is compared with (Sec. 2, after Eq. 2; Sec. 3)
+# --------------------------------------------------------------------------
+def _centre64(vals64) -> np.ndarray:
+    vals64 = [float(v) for v in vals64]
+    total = 0.0
+    for v in vals64:
+        total += v
+    mean = total / len(vals64)
+    return np.array([np.float32(v - mean) for v in vals64], dtype=np.float32)
+
+
+def rank_averaged_qb(z_bits, b, K: int, part_off):
+    """Each shard's exact K/E quantile of its own margins, averaged over the
+    non-empty shards, then centred.  Returns (bhat_p BF16 bits [P,E], a NaN
+    pattern for empty shards; the average [E] binary64; the centred bias)."""
+    z_bits = np.asarray(z_bits, np.uint16)
+    T, E = z_bits.shape
+    part_off = np.asarray(part_off, np.int64)
+    P = part_off.size - 1
+    _, _, tau = _eqb.route_topk(z_bits, b, K)
+    keys = _eqb.margin_keys(z_bits, tau)
+    bhat_p = np.full((P, E), 0x7FC0, np.uint16)      # an empty shard has no quantile (NaN)
+    vals = []
+    for p in range(P):
+        r0, r1 = int(part_off[p]), int(part_off[p + 1])
+        if r1 == r0:
+            continue
+        r_p = _eqb.quantile_rank(r1 - r0, K, E)
+        kstar = _eqb.select_by_sort(keys[r0:r1], r_p)
+        bhat_p[p] = _eqb.kappa_inv(kstar)
+        vals.append(_eqb.bf16_to_f32(bhat_p[p]).astype(np.float64))
+    avg = np.zeros(E, np.float64)
+    for e in range(E):
+        total = 0.0
+        for v in vals:
+            total += float(v[e])
+        avg[e] = total / len(vals)
+    return bhat_p, avg, _centre64(avg)
+
+
+def uniform_bins(z_bits, tau, lo: float, hi: float, nbins: int) -> np.ndarray:
+    """Bin index [T,E] of every binary32 margin tau_t - z_{t,e}."""
+    zf = _eqb.bf16_to_f32(z_bits)
+    m = (np.asarray(tau, np.float32)[:, None] - zf).astype(np.float32)
+    lo32, hi32 = np.float32(lo), np.float32(hi)
+    scale = np.float32(np.float32(nbins) / np.float32(hi32 - lo32))
+    x = ((m - lo32).astype(np.float32) * scale).astype(np.float32)
+    return np.clip(np.floor(x), 0, nbins - 1).astype(np.int64)
+
+
+def histogram_qb(z_bits, b, K: int, part_off, lo: float, hi: float, nbins: int):
+    """Fixed-resolution global-histogram estimate of the K/E quantile.
+    Returns (per-partition counts [P,E,nbins], estimate [E] binary64, the
+    centred bias)."""
+    z_bits = np.asarray(z_bits, np.uint16)
+    T, E = z_bits.shape
+    part_off = np.asarray(part_off, np.int64)
+    P = part_off.size - 1
+    _, _, tau = _eqb.route_topk(z_bits, b, K)
+    bins = uniform_bins(z_bits, tau, lo, hi, nbins)
+    counts = np.zeros((P, E, nbins), np.int64)
+    for p in range(P):
+        r0, r1 = int(part_off[p]), int(part_off[p + 1])
+        for e in range(E):
+            counts[p, e] = np.bincount(bins[r0:r1, e], minlength=nbins)
+    total = counts.sum(axis=0)
+    r = _eqb.quantile_rank(T, K, E)
+    lo64 = float(np.float32(lo))
+    width = (float(np.float32(hi)) - lo64) / nbins
+    est = np.zeros(E, np.float64)
+    for e in range(E):
+        run = np.cumsum(total[e])
+        j = int(np.searchsorted(run, r))          # first bin whose running count reaches r
+        before = int(run[j - 1]) if j > 0 else 0
+        est[e] = lo64 + (j + (r - before) / int(total[e, j])) * width
+    return counts, est, _centre64(est)

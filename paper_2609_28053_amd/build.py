@@ -11,7 +11,7 @@ import sys
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
-SOURCES = [os.path.join(CSRC, f) for f in ("eqb_api.hip", "route.hip", "margin.hip", "select.hip", "balance.hip")]
+SOURCES = [os.path.join(CSRC, f) for f in ("eqb_api.hip", "route.hip", "margin.hip", "select.hip", "balance.hip", "variants.hip")]
 OUT = os.path.join(HERE, "libeqb.so")
 ARCH = os.environ.get("EQB_OFFLOAD_ARCH", "gfx950")
 

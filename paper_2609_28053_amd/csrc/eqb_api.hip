@@ -128,6 +128,86 @@ eqb_status eqb_expert_load(const int32_t* topk_idx, int64_t T, int32_t K, int32_
   return launch_load(topk_idx, T, K, E, load, pt, static_cast<hipStream_t>(stream));
 }
 
+eqb_status eqb_select_quantile_local(int32_t pass, const int32_t* hist, int64_t T, int32_t K, int32_t E,
+                                     const int64_t* part_off, int32_t P, int32_t* sel_hi,
+                                     int64_t* rank_in_bin, int32_t* sel_lo, uint16_t* q_bf16,
+                                     int32_t* dev_status, void* stream) {
+  if (pass != 1 && pass != 2) return EQB_ERR_INVALID_ARG;
+  if (T < 0 || T > INT32_MAX || K < 1 || K >= E) return EQB_ERR_INVALID_ARG;
+  if (!supported_E(E)) return EQB_ERR_UNSUPPORTED;
+  PartTable pt;
+  const eqb_status st = make_table(part_off, P, T, &pt);
+  if (st != EQB_OK) return st;
+  if (!hist || !sel_hi || !rank_in_bin) return EQB_ERR_INVALID_ARG;
+  if (pass == 2 && (!sel_lo || !q_bf16)) return EQB_ERR_INVALID_ARG;
+  return launch_select_local(pass, hist, E, K, pt, sel_hi, rank_in_bin, sel_lo, q_bf16, dev_status,
+                             static_cast<hipStream_t>(stream));
+}
+
+eqb_status eqb_margin_hist_pass2_local(const uint16_t* z, const float* tau, int64_t T, int32_t E,
+                                       const int32_t* sel_hi, const int64_t* part_off, int32_t P,
+                                       int32_t* hist_lo, void* stream) {
+  if (T < 0 || T > INT32_MAX) return EQB_ERR_INVALID_ARG;
+  if (!supported_E(E)) return EQB_ERR_UNSUPPORTED;
+  MarginArgs a;
+  const eqb_status st = make_table(part_off, P, T, &a.pt);
+  if (st != EQB_OK) return st;
+  if (T == 0) return EQB_OK;
+  if (!z || !tau || !hist_lo || !sel_hi) return EQB_ERR_INVALID_ARG;
+  if (!aligned16(z)) return EQB_ERR_UNSUPPORTED;
+  a.z = z;
+  a.tau = tau;
+  a.T = T;
+  a.E = E;
+  a.sel_hi = sel_hi;
+  a.sel_stride = E;
+  a.hist = hist_lo;
+  return launch_margin(true, a, static_cast<hipStream_t>(stream));
+}
+
+eqb_status eqb_rank_average(const uint16_t* q_bf16, int64_t T, int32_t E, const int64_t* part_off,
+                            int32_t P, double* b_avg, float* b_next, void* stream) {
+  if (T < 0 || T > INT32_MAX) return EQB_ERR_INVALID_ARG;
+  if (!supported_E(E)) return EQB_ERR_UNSUPPORTED;
+  PartTable pt;
+  const eqb_status st = make_table(part_off, P, T, &pt);
+  if (st != EQB_OK) return st;
+  if (!q_bf16 || !b_next) return EQB_ERR_INVALID_ARG;
+  return launch_rank_average(q_bf16, E, pt, b_avg, b_next, static_cast<hipStream_t>(stream));
+}
+
+eqb_status eqb_margin_hist_uniform(const uint16_t* z, const float* tau, int64_t T, int32_t E,
+                                   const int64_t* part_off, int32_t P, float lo, float hi, int32_t nbins,
+                                   int32_t* hist, void* stream) {
+  if (T < 0 || T > INT32_MAX) return EQB_ERR_INVALID_ARG;
+  if (!supported_E(E)) return EQB_ERR_UNSUPPORTED;
+  if (nbins < 1 || nbins > EQB_NBINS) return EQB_ERR_INVALID_ARG;
+  const float width = hi - lo;
+  if (!(width > 0.0f) || width > 3.4e38f || !(lo == lo)) return EQB_ERR_INVALID_ARG;
+  const float scale = (float)nbins / width;
+  PartTable pt;
+  const eqb_status st = make_table(part_off, P, T, &pt);
+  if (st != EQB_OK) return st;
+  if (T == 0) return EQB_OK;
+  if (!z || !tau || !hist) return EQB_ERR_INVALID_ARG;
+  if (!aligned16(z)) return EQB_ERR_UNSUPPORTED;
+  return launch_uniform_hist(z, tau, T, E, pt, lo, scale, nbins, hist, static_cast<hipStream_t>(stream));
+}
+
+eqb_status eqb_select_uniform(const int32_t* hist, int32_t P, int32_t E, int32_t nbins, int64_t r, float lo,
+                              float hi, double* est, float* b_next, int32_t* dev_status, void* stream) {
+  if (P < 1 || P > EQB_MAX_PARTITIONS) return EQB_ERR_INVALID_ARG;
+  if (!supported_E(E)) return EQB_ERR_UNSUPPORTED;
+  if (nbins < 1 || nbins > EQB_NBINS) return EQB_ERR_INVALID_ARG;
+  if (!(hi - lo > 0.0f) || !(lo == lo)) return EQB_ERR_INVALID_ARG;
+  if (r < 1 || r > INT32_MAX) return EQB_ERR_RANK;
+  if (!hist || !est) return EQB_ERR_INVALID_ARG;
+  const double lo64 = (double)lo;
+  const double width = ((double)hi - lo64) / (double)nbins;
+  return launch_select_uniform(hist, P, E, nbins, r, lo64, width, est, b_next, dev_status,
+                               static_cast<hipStream_t>(stream));
+}
+
 eqb_status eqb_max_violation(const int32_t* load, int64_t T, int32_t K, int32_t E,
                              const int64_t* part_off, int32_t P, double* maxvio_global,
                              double* maxvio_local, void* stream) {

@@ -24,6 +24,7 @@ struct MarginArgs {
   int64_t T;
   int E;
   const int32_t* sel_hi;   // fine pass only
+  int sel_stride = 0;      // 0: one selection for all partitions; E: one per partition
   int32_t* hist;
   PartTable pt;
 };
@@ -36,6 +37,15 @@ eqb_status launch_select(int pass, const int32_t* hist, int P, int E, int64_t r,
                          int64_t* rank_in_bin, int32_t* sel_lo, uint16_t* q_bf16, float* b_next,
                          int32_t* hist_sum, int32_t* status, hipStream_t s);
 
+eqb_status launch_select_local(int pass, const int32_t* hist, int E, int K, const PartTable& pt,
+                               int32_t* sel_hi, int64_t* rank_in_bin, int32_t* sel_lo, uint16_t* q_bf16,
+                               int32_t* status, hipStream_t s);
+eqb_status launch_rank_average(const uint16_t* q_bf16, int E, const PartTable& pt, double* b_avg,
+                               float* b_next, hipStream_t s);
+eqb_status launch_uniform_hist(const uint16_t* z, const float* tau, int64_t T, int E, const PartTable& pt,
+                               float lo, float scale, int nbins, int32_t* hist, hipStream_t s);
+eqb_status launch_select_uniform(const int32_t* hist, int P, int E, int nbins, int64_t r, double lo,
+                                 double width, double* est, float* b_next, int32_t* status, hipStream_t s);
 eqb_status launch_max_violation(const int32_t* load, int E, int K, const PartTable& pt,
                                 double* out_global, double* out_local, hipStream_t s);
 

@@ -40,10 +40,13 @@ __device__ __forceinline__ void count_piece(uint32_t* sh, const uint4& w, float 
   }
 }
 
+// sel_stride = 0: every partition uses the selection sel_hi[e] (EQB: the
+// bins chosen from the summed counts).  sel_stride = E: partition p uses its
+// own selection sel_hi[p*E + e] (each shard's own quantile).
 template <int E, bool kFine>
 __global__ __launch_bounds__(kBlock) void margin_hist_kernel(
     const uint16_t* __restrict__ z, const float* __restrict__ tau, int64_t T,
-    const int32_t* __restrict__ sel_hi, int32_t* __restrict__ hist, const PartTable pt,
+    const int32_t* __restrict__ sel_hi, int sel_stride, int32_t* __restrict__ hist, const PartTable pt,
     int64_t rows_per_block) {
   constexpr int G = E / 8;
   constexpr int R = 64 / G;
@@ -54,18 +57,6 @@ __global__ __launch_bounds__(kBlock) void margin_hist_kernel(
   const int g = lane % G, rr = lane / G;
   const int e0 = g * 8;
   const uint32_t row0 = hist_row(e0);
-  uint32_t csel[4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    uint32_t c = 0;
-    if (kFine) {
-      int u0 = sel_hi[e0 + 2 * i], u1 = sel_hi[e0 + 2 * i + 1];
-      u0 = (u0 >= 0 && u0 < kNBins) ? u0 : 0;   // invalid selections are skipped at the flush
-      u1 = (u1 >= 0 && u1 < kNBins) ? u1 : 0;
-      c = ((uint32_t)raw_hi_of_kappa(u1) << 24) | ((uint32_t)raw_hi_of_kappa(u0) << 8);
-    }
-    csel[i] = c;
-  }
   for (int w = threadIdx.x; w < hist_words<E>(); w += kBlock) sh_hist[w] = 0;
   __syncthreads();
 
@@ -75,6 +66,19 @@ __global__ __launch_bounds__(kBlock) void margin_hist_kernel(
   // reads every block range first to last, so the rows it read last may still
   // be held by the memory-side cache.
   for_each_segment_rev(r0, r1, pt, [&](int p, int64_t s0, int64_t s1) {
+    const int32_t* sel = kFine ? sel_hi + (int64_t)p * sel_stride : nullptr;
+    uint32_t csel[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      uint32_t c = 0;
+      if (kFine) {
+        int u0 = sel[e0 + 2 * i], u1 = sel[e0 + 2 * i + 1];
+        u0 = (u0 >= 0 && u0 < kNBins) ? u0 : 0;   // invalid selections are skipped at the flush
+        u1 = (u1 >= 0 && u1 < kNBins) ? u1 : 0;
+        c = ((uint32_t)raw_hi_of_kappa(u1) << 24) | ((uint32_t)raw_hi_of_kappa(u0) << 8);
+      }
+      csel[i] = c;
+    }
     uint4 va[kMarginU], vb[kMarginU];
     float ta[kMarginU], tb[kMarginU];
     // rows of a step: u * kWaves * R + wave * R + rr; invalid rows read nothing
@@ -121,7 +125,7 @@ __global__ __launch_bounds__(kBlock) void margin_hist_kernel(
           for (int h = 0; h < 2; ++h) {
             const uint32_t n = h ? (c >> 16) : (c & 0xFFFFu);
             const int e = 2 * pair + h;
-            const int u = sel_hi[e];
+            const int u = sel[e];
             if (n && u >= 0 && u < kNBins)
               atomicAdd(slab + e * kNBins + ((u < 0x80) ? (lr ^ 0xFF) : lr), (int32_t)n);
           }
@@ -140,9 +144,10 @@ eqb_status launch_margin_e(bool fine, const MarginArgs& a, hipStream_t s) {
   const int rows_per_step = kWaves * (64 / (E / 8)) * kMarginU;
   grid_for(a.T, rows_per_step, hist_words<E>() * 4 * 2 <= 160 * 1024 ? 2 : 1, &blocks, &rpb);
   if (fine)
-    margin_hist_kernel<E, true><<<blocks, kBlock, 0, s>>>(a.z, a.tau, a.T, a.sel_hi, a.hist, a.pt, rpb);
+    margin_hist_kernel<E, true><<<blocks, kBlock, 0, s>>>(a.z, a.tau, a.T, a.sel_hi, a.sel_stride, a.hist,
+                                                         a.pt, rpb);
   else
-    margin_hist_kernel<E, false><<<blocks, kBlock, 0, s>>>(a.z, a.tau, a.T, a.sel_hi, a.hist, a.pt, rpb);
+    margin_hist_kernel<E, false><<<blocks, kBlock, 0, s>>>(a.z, a.tau, a.T, a.sel_hi, 0, a.hist, a.pt, rpb);
   return launch_status();
 }
 

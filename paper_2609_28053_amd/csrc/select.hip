@@ -20,47 +20,82 @@ __device__ __forceinline__ int64_t block_inclusive_scan_256(int64_t x, int64_t* 
   return sh[i];
 }
 
-// One block per expert, one thread per bin.
+// One block per expert (and, with kLocal, per partition), one thread per bin.
+// Global: the P slabs are summed first (the all-reduce) and r is the rank over
+// the whole batch.  kLocal: slab p alone, with its own rank
+// r_p = ceil(|B_p| K / E), written to entry [p, e]; an empty partition has no
+// quantile and gets -1 without raising the status.
+template <bool kLocal>
 __global__ __launch_bounds__(kNBins) void select_coarse_kernel(
-    const int32_t* __restrict__ hist, int P, int E, int64_t r, int32_t* __restrict__ sel_hi,
-    int64_t* __restrict__ rank_in_bin, int32_t* __restrict__ hist_sum, int32_t* __restrict__ status) {
+    const int32_t* __restrict__ hist, int P, int E, int K, int64_t r, const PartTable pt,
+    int32_t* __restrict__ sel_hi, int64_t* __restrict__ rank_in_bin, int32_t* __restrict__ hist_sum,
+    int32_t* __restrict__ status) {
   __shared__ int64_t sh[kNBins];
-  const int e = blockIdx.x, u = threadIdx.x;
+  const int e = blockIdx.x, u = threadIdx.x, p = kLocal ? (int)blockIdx.y : 0;
+  const int64_t out = kLocal ? (int64_t)p * E + e : e;
+  if (kLocal) {
+    const int64_t n = pt.off[p + 1] - pt.off[p];
+    if (n == 0) {
+      if (u == 0) {
+        sel_hi[out] = -1;
+        rank_in_bin[out] = 0;
+      }
+      return;
+    }
+    r = (n * K + E - 1) / E;
+  }
   int64_t c = 0;
-  for (int p = 0; p < P; ++p) c += hist[((int64_t)p * E + e) * kNBins + u];
-  if (hist_sum) hist_sum[(int64_t)e * kNBins + u] = (int32_t)c;
+  if (kLocal) {
+    c = hist[((int64_t)p * E + e) * kNBins + u];
+  } else {
+    for (int q = 0; q < P; ++q) c += hist[((int64_t)q * E + e) * kNBins + u];
+    if (hist_sum) hist_sum[(int64_t)e * kNBins + u] = (int32_t)c;
+  }
   const int64_t cum = block_inclusive_scan_256(c, sh);
   if (cum >= r && cum - c < r) {
-    sel_hi[e] = u;
-    rank_in_bin[e] = r - (cum - c);
+    sel_hi[out] = u;
+    rank_in_bin[out] = r - (cum - c);
   }
   if (u == kNBins - 1 && cum < r) {
-    sel_hi[e] = -1;
-    rank_in_bin[e] = 0;
+    sel_hi[out] = -1;
+    rank_in_bin[out] = 0;
     if (status) *status = EQB_DEV_RANK_EXCEEDS_COUNT;
   }
 }
 
+template <bool kLocal>
 __global__ __launch_bounds__(kNBins) void select_fine_kernel(
-    const int32_t* __restrict__ hist, int P, int E, const int32_t* __restrict__ sel_hi,
+    const int32_t* __restrict__ hist, int P, int E, const PartTable pt, const int32_t* __restrict__ sel_hi,
     const int64_t* __restrict__ rank_in_bin, int32_t* __restrict__ sel_lo,
     uint16_t* __restrict__ q_bf16, int32_t* __restrict__ hist_sum, int32_t* __restrict__ status) {
   __shared__ int64_t sh[kNBins];
-  const int e = blockIdx.x, v = threadIdx.x;
+  const int e = blockIdx.x, v = threadIdx.x, p = kLocal ? (int)blockIdx.y : 0;
+  const int64_t out = kLocal ? (int64_t)p * E + e : e;
+  if (kLocal && pt.off[p + 1] == pt.off[p]) {
+    if (v == 0) {
+      sel_lo[out] = -1;
+      q_bf16[out] = 0x7FC0;
+    }
+    return;
+  }
   int64_t c = 0;
-  for (int p = 0; p < P; ++p) c += hist[((int64_t)p * E + e) * kNBins + v];
-  if (hist_sum) hist_sum[(int64_t)e * kNBins + v] = (int32_t)c;
+  if (kLocal) {
+    c = hist[((int64_t)p * E + e) * kNBins + v];
+  } else {
+    for (int q = 0; q < P; ++q) c += hist[((int64_t)q * E + e) * kNBins + v];
+    if (hist_sum) hist_sum[(int64_t)e * kNBins + v] = (int32_t)c;
+  }
   const int64_t cum = block_inclusive_scan_256(c, sh);
-  const int u = sel_hi[e];
-  const int64_t rho = rank_in_bin[e];
+  const int u = sel_hi[out];
+  const int64_t rho = rank_in_bin[out];
   const bool ok = u >= 0 && u < kNBins && rho >= 1;
   if (ok && cum >= rho && cum - c < rho) {
-    sel_lo[e] = v;
-    q_bf16[e] = kappa_inv(((uint32_t)u << 8) | (uint32_t)v);
+    sel_lo[out] = v;
+    q_bf16[out] = kappa_inv(((uint32_t)u << 8) | (uint32_t)v);
   }
   if (v == kNBins - 1 && (!ok || cum < rho)) {
-    sel_lo[e] = -1;
-    q_bf16[e] = 0x7FC0;
+    sel_lo[out] = -1;
+    q_bf16[out] = 0x7FC0;
     if (status) *status = EQB_DEV_RANK_EXCEEDS_COUNT;
   }
 }
@@ -85,17 +120,34 @@ __global__ __launch_bounds__(256) void center_kernel(const uint16_t* __restrict_
 eqb_status launch_select(int pass, const int32_t* hist, int P, int E, int64_t r, int32_t* sel_hi,
                          int64_t* rank_in_bin, int32_t* sel_lo, uint16_t* q_bf16, float* b_next,
                          int32_t* hist_sum, int32_t* status, hipStream_t s) {
+  PartTable none{};
+  none.P = P;
   if (pass == 1) {
-    select_coarse_kernel<<<E, kNBins, 0, s>>>(hist, P, E, r, sel_hi, rank_in_bin, hist_sum, status);
+    select_coarse_kernel<false><<<E, kNBins, 0, s>>>(hist, P, E, 0, r, none, sel_hi, rank_in_bin, hist_sum,
+                                                     status);
     return launch_status();
   }
-  select_fine_kernel<<<E, kNBins, 0, s>>>(hist, P, E, sel_hi, rank_in_bin, sel_lo, q_bf16, hist_sum, status);
+  select_fine_kernel<false><<<E, kNBins, 0, s>>>(hist, P, E, none, sel_hi, rank_in_bin, sel_lo, q_bf16,
+                                                 hist_sum, status);
   if (launch_status() != EQB_OK) return EQB_ERR_HIP;
   if (b_next) {
     center_kernel<<<1, 256, 0, s>>>(q_bf16, E, b_next);
     return launch_status();
   }
   return EQB_OK;
+}
+
+eqb_status launch_select_local(int pass, const int32_t* hist, int E, int K, const PartTable& pt,
+                               int32_t* sel_hi, int64_t* rank_in_bin, int32_t* sel_lo, uint16_t* q_bf16,
+                               int32_t* status, hipStream_t s) {
+  const dim3 grid(E, pt.P);
+  if (pass == 1)
+    select_coarse_kernel<true><<<grid, kNBins, 0, s>>>(hist, pt.P, E, K, 0, pt, sel_hi, rank_in_bin, nullptr,
+                                                       status);
+  else
+    select_fine_kernel<true><<<grid, kNBins, 0, s>>>(hist, pt.P, E, pt, sel_hi, rank_in_bin, sel_lo, q_bf16,
+                                                     nullptr, status);
+  return launch_status();
 }
 
 }  // namespace eqb

@@ -34,6 +34,11 @@ EXPORTS = (
     "eqb_select_quantile",
     "eqb_margin_hist_pass2",
     "eqb_expert_load",
+    "eqb_select_quantile_local",
+    "eqb_margin_hist_pass2_local",
+    "eqb_rank_average",
+    "eqb_margin_hist_uniform",
+    "eqb_select_uniform",
     "eqb_max_violation",
     "eqb_lei_residual",
     "eqb_lei_inject",
@@ -57,6 +62,11 @@ def _load():
         "eqb_select_quantile": [i32, P, i32, i32, i64, P, P, P, P, P, P, P, P],
         "eqb_margin_hist_pass2": [P, P, i64, i32, P, P, i32, P, P],
         "eqb_expert_load": [P, i64, i32, i32, P, i32, P, P],
+        "eqb_select_quantile_local": [i32, P, i64, i32, i32, P, i32, P, P, P, P, P, P],
+        "eqb_margin_hist_pass2_local": [P, P, i64, i32, P, P, i32, P, P],
+        "eqb_rank_average": [P, i64, i32, P, i32, P, P, P],
+        "eqb_margin_hist_uniform": [P, P, i64, i32, P, i32, ctypes.c_float, ctypes.c_float, i32, P, P],
+        "eqb_select_uniform": [P, i32, i32, i32, i64, ctypes.c_float, ctypes.c_float, P, P, P, P],
         "eqb_max_violation": [P, i64, i32, i32, P, i32, P, P, P],
         "eqb_lei_residual": [P, i64, i32, i32, P, i32, ctypes.c_double, ctypes.c_double, P, P],
         "eqb_lei_inject": [P, P, i64, i32, P, i32, P],
@@ -170,6 +180,62 @@ def eqb_expert_load(topk_idx, E, load, part_off=None, stream=None):
         _ptr(topk_idx, torch.int32, T * K, "topk_idx"), T, K, E, po, P,
         _ptr(load, torch.int32, P * E, "load"), _stream(stream)))
     del keep
+
+
+def eqb_select_quantile_local(pass_, hist, T, K, sel_hi, rank_in_bin, sel_lo=None, q_bf16=None,
+                              part_off=None, dev_status=None, stream=None):
+    P, E, nb = hist.shape
+    assert nb == EQB_NBINS
+    po, Pn, keep = _offsets(part_off, T)
+    if Pn != P:
+        raise ValueError(f"hist has {P} partitions, part_off describes {Pn}")
+    _check("eqb_select_quantile_local", lib.eqb_select_quantile_local(
+        pass_, _ptr(hist, torch.int32, name="hist"), T, K, E, po, P,
+        _ptr(sel_hi, torch.int32, P * E, "sel_hi"), _ptr(rank_in_bin, torch.int64, P * E, "rank_in_bin"),
+        _ptr(sel_lo, torch.int32, P * E, "sel_lo"), _ptr(q_bf16, _Z, P * E, "q_bf16"),
+        _ptr(dev_status, torch.int32, 1, "dev_status"), _stream(stream)))
+    del keep
+
+
+def eqb_margin_hist_pass2_local(z, tau, sel_hi, hist_lo, part_off=None, stream=None):
+    T, E = z.shape
+    po, P, keep = _offsets(part_off, T)
+    _check("eqb_margin_hist_pass2_local", lib.eqb_margin_hist_pass2_local(
+        _ptr(z, _Z, name="z"), _ptr(tau, torch.float32, T, "tau"), T, E,
+        _ptr(sel_hi, torch.int32, P * E, "sel_hi"), po, P,
+        _ptr(hist_lo, torch.int32, P * E * EQB_NBINS, "hist_lo"), _stream(stream)))
+    del keep
+
+
+def eqb_rank_average(q_bf16, T, b_next, b_avg=None, part_off=None, stream=None):
+    P, E = q_bf16.shape
+    po, Pn, keep = _offsets(part_off, T)
+    if Pn != P:
+        raise ValueError(f"q_bf16 has {P} partitions, part_off describes {Pn}")
+    _check("eqb_rank_average", lib.eqb_rank_average(
+        _ptr(q_bf16, _Z, P * E, "q_bf16"), T, E, po, P, _ptr(b_avg, torch.float64, E, "b_avg"),
+        _ptr(b_next, torch.float32, E, "b_next"), _stream(stream)))
+    del keep
+
+
+def eqb_margin_hist_uniform(z, tau, lo, hi, hist, part_off=None, stream=None):
+    T, E = z.shape
+    P, E2, nbins = hist.shape
+    po, Pn, keep = _offsets(part_off, T)
+    if Pn != P or E2 != E:
+        raise ValueError("hist must be [P, E, nbins]")
+    _check("eqb_margin_hist_uniform", lib.eqb_margin_hist_uniform(
+        _ptr(z, _Z, name="z"), _ptr(tau, torch.float32, T, "tau"), T, E, po, P, float(lo), float(hi), nbins,
+        _ptr(hist, torch.int32, P * E * nbins, "hist"), _stream(stream)))
+    del keep
+
+
+def eqb_select_uniform(hist, r, lo, hi, est, b_next=None, dev_status=None, stream=None):
+    P, E, nbins = hist.shape
+    _check("eqb_select_uniform", lib.eqb_select_uniform(
+        _ptr(hist, torch.int32, name="hist"), P, E, nbins, r, float(lo), float(hi),
+        _ptr(est, torch.float64, E, "est"), _ptr(b_next, torch.float32, E, "b_next"),
+        _ptr(dev_status, torch.int32, 1, "dev_status"), _stream(stream)))
 
 
 def eqb_max_violation(load, T, K, maxvio_global, maxvio_local=None, part_off=None, stream=None):
@@ -303,3 +369,59 @@ def qb_loop(batches, b0, K: int, part_off=None, stream=None):
                               bhat=lay.q_bf16.cpu().numpy().view(np.uint16), b_next=b.cpu().numpy(),
                               dev_status=int(lay.dev_status.item())))
     return steps
+
+
+def rank_averaged_qb(z, b, K: int, part_off=None, stream=None) -> dict:
+    """Rank-averaged QB (Sec. 2): every shard's exact K/E quantile of its own
+    margins, averaged over the shards and centred.  Returns host copies of
+    the shards' quantiles (BF16 bits [P,E]), the average (binary64 [E]) and
+    the centred bias."""
+    T, E = z.shape
+    P = 1 if part_off is None else len(part_off) - 1
+    ctx = torch.cuda.stream(stream) if stream is not None else contextlib.nullcontext()
+    with ctx:
+        dev = z.device
+        i32 = dict(dtype=torch.int32, device=dev)
+        idx = torch.empty((T, K), **i32)
+        score = torch.empty((T, K), dtype=torch.float32, device=dev)
+        tau = torch.empty(T, dtype=torch.float32, device=dev)
+        hist = torch.zeros((2, P, E, EQB_NBINS), **i32)
+        status = torch.zeros(1, **i32)
+        sel_hi = torch.empty((P, E), **i32)
+        sel_lo = torch.empty((P, E), **i32)
+        rib = torch.empty((P, E), dtype=torch.int64, device=dev)
+        q = torch.empty((P, E), dtype=torch.int16, device=dev)
+        b_avg = torch.empty(E, dtype=torch.float64, device=dev)
+        b_next = torch.empty(E, dtype=torch.float32, device=dev)
+        eqb_route_topk(z, b, K, idx, score, tau, part_off, None, hist[0])
+        eqb_select_quantile_local(1, hist[0], T, K, sel_hi, rib, part_off=part_off, dev_status=status)
+        eqb_margin_hist_pass2_local(z, tau, sel_hi, hist[1], part_off)
+        eqb_select_quantile_local(2, hist[1], T, K, sel_hi, rib, sel_lo, q, part_off, status)
+        eqb_rank_average(q, T, b_next, b_avg, part_off)
+        return dict(bhat_p=q.cpu().numpy().view(np.uint16), b_avg=b_avg.cpu().numpy(),
+                    b_next=b_next.cpu().numpy(), dev_status=int(status.item()))
+
+
+def histogram_qb(z, b, K: int, lo: float, hi: float, nbins: int, part_off=None, stream=None) -> dict:
+    """Fixed-resolution histogram QB (Sec. 2): margin counts over nbins
+    uniform bins of [lo, hi), summed over the shards, the K/E quantile read
+    off the sum by linear interpolation within its bin, then centred.
+    Returns host copies of the counts [P,E,nbins], the estimate (binary64 [E])
+    and the centred bias."""
+    T, E = z.shape
+    P = 1 if part_off is None else len(part_off) - 1
+    ctx = torch.cuda.stream(stream) if stream is not None else contextlib.nullcontext()
+    with ctx:
+        dev = z.device
+        idx = torch.empty((T, K), dtype=torch.int32, device=dev)
+        score = torch.empty((T, K), dtype=torch.float32, device=dev)
+        tau = torch.empty(T, dtype=torch.float32, device=dev)
+        hist = torch.zeros((P, E, nbins), dtype=torch.int32, device=dev)
+        status = torch.zeros(1, dtype=torch.int32, device=dev)
+        est = torch.empty(E, dtype=torch.float64, device=dev)
+        b_next = torch.empty(E, dtype=torch.float32, device=dev)
+        eqb_route_topk(z, b, K, idx, score, tau, part_off)
+        eqb_margin_hist_uniform(z, tau, lo, hi, hist, part_off)
+        eqb_select_uniform(hist, eqb_rank(T, K, E), lo, hi, est, b_next, status)
+        return dict(counts=hist.cpu().numpy(), est=est.cpu().numpy(), b_next=b_next.cpu().numpy(),
+                    dev_status=int(status.item()))

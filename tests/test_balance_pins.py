@@ -222,3 +222,118 @@ def test_lei_pins_catch_planted_mistakes(monkeypatch, mutant):
             failed = True
     assert failed, mutant
     del orig
+
+
+# ------------------------------------- statistics EQB is compared with --------
+from oracle import eqb_oracle as O
+
+
+def test_rank_average_of_one_shard_is_eqb():
+    w = W.CONFIGS["skew64"].with_T(6000, 1)
+    z, b, off = W.generate(w)
+    bp, avg, bn = B.rank_averaged_qb(z, b, w.K, off)
+    ex = O.run_layer(z, b, w.K, off)
+    np.testing.assert_array_equal(bp[0], ex["bhat"])
+    np.testing.assert_array_equal(bn.view(np.uint32), ex["b_next"].view(np.uint32))
+
+
+def test_rank_average_of_identical_shards_is_eqb():
+    """P copies of one batch: every shard's quantile is the global one."""
+    w = W.CONFIGS["skew64"].with_T(2048, 1)        # 2048 * 6 / 64 is an integer
+    z, b, _ = W.generate(w)
+    zz = np.concatenate([z] * 3)
+    off = np.array([0, 2048, 4096, 6144])
+    bp, avg, bn = B.rank_averaged_qb(zz, b, w.K, off)
+    ex = O.run_layer(zz, b, w.K, off)
+    for p in range(3):
+        np.testing.assert_array_equal(bp[p], ex["bhat"])
+    np.testing.assert_array_equal(bn.view(np.uint32), ex["b_next"].view(np.uint32))
+
+
+def test_shard_quantile_is_numpys_inverted_cdf_and_average_depends_on_the_split():
+    w = W.CONFIGS["skew64"].with_T(9000, 3)
+    z, b, off = W.generate(w)
+    bp, avg, _ = B.rank_averaged_qb(z, b, w.K, off)
+    _, _, tau = O.route_topk(z, b, w.K)
+    m = O.bf16_to_f32(O.kappa_inv(O.margin_keys(z, tau))).astype(np.float64)
+    for p in range(3):
+        sl = m[off[p]:off[p + 1]]
+        q = np.quantile(sl, w.K / w.E, axis=0, method="inverted_cdf")
+        np.testing.assert_array_equal(O.bf16_to_f32(bp[p]).astype(np.float64), q)
+    np.testing.assert_array_equal(avg, (O.bf16_to_f32(bp).astype(np.float64).sum(0)) / 3)
+    # another split of the same batch gives another average (Sec. 2: partition dependent)
+    _, avg2, _ = B.rank_averaged_qb(z, b, w.K, [0, 1000, 9000])
+    assert np.any(avg2 != avg)
+
+
+def test_rank_average_skips_empty_shards():
+    w = W.CONFIGS["skew64"].with_T(4000, 2)
+    z, b, _ = W.generate(w)
+    bp, avg, _ = B.rank_averaged_qb(z, b, w.K, [0, 2000, 2000, 4000])
+    assert np.all(bp[1] == 0x7FC0)
+    np.testing.assert_array_equal(avg, (O.bf16_to_f32(bp[[0, 2]]).astype(np.float64).sum(0)) / 2)
+
+
+def test_uniform_bins_against_exact_rationals():
+    rng = np.random.default_rng(2)
+    T, E = 300, 8
+    z = O.f32_to_bf16_rne((rng.standard_normal((T, E)) * 2).astype(np.float32))
+    tau = (rng.standard_normal(T) * 2).astype(np.float32)
+    lo, hi, nb = -6.0, 6.0, 37
+    bins = B.uniform_bins(z, tau, lo, hi, nb)
+    m = (tau[:, None] - O.bf16_to_f32(z)).astype(np.float32)
+    for t in range(T):
+        for e in range(E):
+            x = (Fraction(float(m[t, e])) - Fraction(lo)) * nb / (Fraction(hi) - Fraction(lo))
+            j = min(max(math.floor(x), 0), nb - 1)
+            if abs(x - round(x)) > Fraction(1, 10 ** 4):        # away from bin edges
+                assert bins[t, e] == j
+
+
+def test_histogram_estimate_lies_in_the_bin_of_the_exact_quantile():
+    w = W.CONFIGS["skew64"].with_T(9000, 3)
+    z, b, off = W.generate(w)
+    lo, hi, nb = -10.0, 10.0, 200
+    counts, est, bn = B.histogram_qb(z, b, w.K, off, lo, hi, nb)
+    assert np.all(counts.sum(axis=2) == np.diff(off)[:, None])
+    _, _, tau = O.route_topk(z, b, w.K)
+    m = np.sort((tau[:, None] - O.bf16_to_f32(z)).astype(np.float32), axis=0)
+    r = O.quantile_rank(w.T, w.K, w.E)
+    exact = m[r - 1].astype(np.float64)
+    width = (hi - lo) / nb
+    assert np.all(np.abs(est - exact) <= width)
+    jb = B.uniform_bins(z, tau, lo, hi, nb)
+    j = np.array([jb[np.argsort((tau - O.bf16_to_f32(z[:, e])).astype(np.float32), kind="stable")[r - 1], e]
+                  for e in range(w.E)])
+    assert np.all(est >= lo + j * width - 1e-12) and np.all(est <= lo + (j + 1) * width + 1e-12)
+    assert abs(float(bn.astype(np.float64).sum())) < 1e-3
+
+
+@pytest.mark.parametrize("mutant", ["divide_by_all_shards", "interp_after_bin"])
+def test_variant_pins_catch_planted_mistakes(monkeypatch, mutant):
+    if mutant == "divide_by_all_shards":
+        orig = B.rank_averaged_qb
+
+        def bad(z_bits, b, K, part_off):
+            bp, avg, bn = orig(z_bits, b, K, part_off)
+            P = len(part_off) - 1
+            vals = np.where(bp == 0x7FC0, 0.0, O.bf16_to_f32(bp).astype(np.float64))
+            avg = vals.sum(0) / P
+            return bp, avg, bn
+        monkeypatch.setattr(B, "rank_averaged_qb", bad)
+        fns = (test_rank_average_skips_empty_shards,)
+    else:
+        orig_hq = B.histogram_qb
+
+        def bad(z_bits, b, K, part_off, lo, hi, nbins):
+            counts, est, bn = orig_hq(z_bits, b, K, part_off, lo, hi, nbins)
+            return counts, est + (hi - lo) / nbins, bn        # reads the quantile one bin too high
+        monkeypatch.setattr(B, "histogram_qb", bad)
+        fns = (test_histogram_estimate_lies_in_the_bin_of_the_exact_quantile,)
+    failed = False
+    for fn in fns:
+        try:
+            fn()
+        except AssertionError:
+            failed = True
+    assert failed, mutant
