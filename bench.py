@@ -41,12 +41,16 @@ def pass_bytes_per_token(E, K):
     return 4 * E + 8 * K + 8
 
 
+ROUTE_SOURCES = [os.path.join(CSRC, f) for f in ("route.hip", "eqb_device.hpp", "eqb_internal.hpp")] + \
+    [os.path.join(ROOT, "include", "eqb.h")]
+
+
 def source_hash():
-    """Hash of every kernel source; counters taken on other sources are stale."""
+    """Hash of the route kernel's sources; counters taken on other sources are stale."""
     h = hashlib.sha256()
-    for name in sorted(os.listdir(CSRC)):
-        with open(os.path.join(CSRC, name), "rb") as f:
-            h.update(name.encode() + b"\0" + f.read())
+    for path in ROUTE_SOURCES:
+        with open(path, "rb") as f:
+            h.update(os.path.basename(path).encode() + b"\0" + f.read())
     return h.hexdigest()[:16]
 
 

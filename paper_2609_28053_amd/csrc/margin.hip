@@ -79,35 +79,36 @@ __global__ __launch_bounds__(kBlock) void margin_hist_kernel(
       }
       csel[i] = c;
     }
+    // Rows are addressed by 32-bit byte offsets from the segment's first row
+    // (a segment holds at most kSegMax rows).  The next step's rows are in
+    // flight while a step is counted; each step starts by taking the rows
+    // prefetched one step earlier.  A row past the segment reads the
+    // segment's last row instead and is not counted.
     uint4 va[kMarginU], vb[kMarginU];
     float ta[kMarginU], tb[kMarginU];
-    // rows of a step: u * kWaves * R + wave * R + rr; invalid rows read nothing
-    auto load_step = [&](uint4 (&v)[kMarginU], float (&tv)[kMarginU], int64_t base) {
+    const char* seg_z = reinterpret_cast<const char*>(z + s0 * E);
+    const char* seg_tau = reinterpret_cast<const char*>(tau + s0);
+    const uint32_t n = (uint32_t)(s1 - s0);
+    auto load_step = [&](uint4 (&v)[kMarginU], float (&tv)[kMarginU], uint32_t base) {
 #pragma unroll
       for (int u = 0; u < kMarginU; ++u) {
-        const int64_t t = base + (int64_t)(u * kWaves + wave) * R + rr;
-        v[u] = make_uint4(0, 0, 0, 0);
-        tv[u] = 0.0f;
-        if (t < s1) {
-          v[u] = *reinterpret_cast<const uint4*>(z + t * E + e0);
-          tv[u] = tau[t];
-        }
+        uint32_t t = base + (uint32_t)((u * kWaves + wave) * R + rr);
+        t = t < n ? t : n - 1;
+        v[u] = *reinterpret_cast<const uint4*>(seg_z + (t * (uint32_t)E + (uint32_t)e0) * 2u);
+        tv[u] = *reinterpret_cast<const float*>(seg_tau + t * 4u);
       }
     };
-    // the next step's rows are in flight while a step is counted
-    const int64_t last = s0 + ((s1 - 1 - s0) / ROWS) * ROWS;
-    load_step(va, ta, last);
-    for (int64_t base = last; base >= s0; base -= ROWS) {
-      if (base - ROWS >= s0) load_step(vb, tb, base - ROWS);
+    const uint32_t last = ((n - 1) / ROWS) * ROWS;
+    load_step(vb, tb, last);
+    for (uint32_t step = 0; step <= last / ROWS; ++step) {
+      const uint32_t base = last - step * ROWS;
+#pragma unroll
+      for (int u = 0; u < kMarginU; ++u) { va[u] = vb[u]; ta[u] = tb[u]; }
+      if (base >= ROWS) load_step(vb, tb, base - ROWS);
 #pragma unroll
       for (int u = 0; u < kMarginU; ++u) {
-        const int64_t t = base + (int64_t)(u * kWaves + wave) * R + rr;
-        if (t < s1) count_piece<kFine>(sh_hist, va[u], ta[u], row0, csel);
-      }
-#pragma unroll
-      for (int u = 0; u < kMarginU; ++u) {
-        va[u] = vb[u];
-        ta[u] = tb[u];
+        const uint32_t t = base + (uint32_t)((u * kWaves + wave) * R + rr);
+        if (t < n) count_piece<kFine>(sh_hist, va[u], ta[u], row0, csel);
       }
     }
     __syncthreads();

@@ -31,15 +31,38 @@ template <int E> struct FastCfg { static constexpr int G = E >= 64 ? 8 : E / 8; 
 // adjacent BF16 values give scores more than 256 binary32 ulps of s apart,
 // so at most one BF16 value maps to H; it is bf16(s_mid - b) with s_mid the
 // middle of the 256-ulp interval, and it is accepted only after
-// fl32(z + b) is checked to reproduce H.  Otherwise z is read from memory.
-__device__ __forceinline__ uint32_t z_from_key(int key, float b, const uint16_t* zptr) {
+// fl32(z + b) is checked to reproduce H.  *ok reports the check; otherwise z
+// must be read from memory (z_or_load).
+__device__ __forceinline__ uint32_t z_from_key(int key, float b, bool* ok) {
   const uint32_t kb = (uint32_t)key;
   const float s_mid = __uint_as_float((kb & 0xFFFFFF00u) | 0x80u);
   const uint32_t zc = bf16x2_bits(s_mid - b, 0.0f) & 0xFFFFu;
   const uint32_t sc = __float_as_uint(__uint_as_float(zc << 16) + b);
   const int ez = (int)((zc >> 7) & 0xFFu), es = (int)((kb >> 23) & 0xFFu);
-  const bool ok = ((sc ^ kb) < 256u) && (ez >= es - 6) && ((zc & 0x7F80u) != 0x7F80u);
-  return ok ? zc : (uint32_t)*zptr;
+  *ok = ((sc ^ kb) < 256u) && (ez >= es - 6) && ((zc & 0x7F80u) != 0x7F80u);
+  return zc;
+}
+
+// Replaces the recovered z by the stored one where the recovery failed.  The
+// load and its use sit inside a branch the whole wave takes or skips, so the
+// common case carries no pending load (and no wait that would also drain the
+// prefetched rows).
+__device__ __forceinline__ uint32_t z_or_load(uint32_t zc, bool ok, const uint16_t* zptr) {
+  if (__builtin_expect(__any(!ok), 0)) {
+    uint32_t zl = zc;
+    if (!ok) zl = *zptr;
+    zc = zl | 0u;
+    __builtin_amdgcn_s_waitcnt(0);
+  }
+  return zc;
+}
+
+// Element at a 32-bit byte offset from a (wave-uniform) base pointer: the
+// form the loads and stores take as a 64-bit scalar base plus a 32-bit
+// vector offset.
+template <class V, class B>
+__device__ __forceinline__ V& at(B* base, uint32_t byte_off) {
+  return *reinterpret_cast<V*>(reinterpret_cast<char*>(const_cast<std::remove_const_t<B>*>(base)) + byte_off);
 }
 
 // Insert x into the sorted list L[0] >= ... >= L[n-1] (one max, n-1 med3).
@@ -116,7 +139,16 @@ __global__ __launch_bounds__(kBlock) void route_fast_kernel(
     }
   };
 
-  auto process = [&](const uint2 (&raw)[NQ], int64_t t, bool valid) __attribute__((always_inline)) {
+  // Base pointers of the current segment (at most kSegMax rows): rows are
+  // addressed by a 32-bit offset from them, which the loads and stores take
+  // directly next to a wave-uniform 64-bit base.
+  const uint16_t* seg_z = z;
+  int32_t* seg_idx = topk_idx;
+  float* seg_score = topk_score;
+  float* seg_tau = tau;
+
+  // t: row index inside the current segment
+  auto process = [&](const uint2 (&raw)[NQ], uint32_t t, bool valid) __attribute__((always_inline)) {
     // ---- widen the logits once; build keys and the per-lane sorted list
     float zf[N];
 #pragma unroll
@@ -174,10 +206,14 @@ __global__ __launch_bounds__(kBlock) void route_fast_kernel(
 #pragma unroll
       for (int s = 0; s < RSLOT; ++s) {
         const int k = s * G + g;
+        bool ok = true;
+        uint32_t zc = 0;
+        int e = 0;
         if (valid && k <= KT) {
-          const int e = 255 - (rk[s] & 0xFF);
-          zown[s] = z_from_key(rk[s], sh_b[e], z + t * E + e);
+          e = 255 - (rk[s] & 0xFF);
+          zc = z_from_key(rk[s], sh_b[e], &ok);
         }
+        zown[s] = z_or_load(zc, ok, &at<uint16_t>(seg_z, (t * E + e) * 2u));
       }
       const int tauhi = mK >> 8;
       const bool dry = group_max_i32<G>((int)(L[0] == INT_MIN)) != 0;
@@ -225,7 +261,9 @@ __global__ __launch_bounds__(kBlock) void route_fast_kernel(
             const int key = (int)myrank[k].x;
             const int e = 255 - (key & 0xFF);
             const float bv = sh_b[e];
-            const uint32_t zb = z_from_key(key, bv, z + t * E + e);
+            bool ok;
+            uint32_t zb = z_from_key(key, bv, &ok);
+            if (!ok) zb = seg_z[t * E + e];
             const uint32_t sb = __float_as_uint(__uint_as_float(zb << 16) + bv);
             myrank[k] = make_uint2(sb, (zb << 16) | (uint32_t)e);
           }
@@ -263,7 +301,7 @@ __global__ __launch_bounds__(kBlock) void route_fast_kernel(
         const int k = s * G + g;
         if (staged && k < nrank) {
           const int e = 255 - (int)(myrank[k].x & 0xFF);
-          const uint32_t zb = z[t * E + e];
+          const uint32_t zb = seg_z[t * E + e];
           const uint32_t sb = __float_as_uint(__uint_as_float(zb << 16) + sh_b[e]);
           myrank[k] = make_uint2(sb, (zb << 16) | (uint32_t)e);
         }
@@ -341,8 +379,8 @@ __global__ __launch_bounds__(kBlock) void route_fast_kernel(
           const int e = 255 - (rk[s] & 0xFF);
           const uint32_t zb = zown[s];
           if (k < K) {
-            topk_idx[t * K + k] = e;
-            topk_score[t * K + k] = sigmoid_fast(__uint_as_float(zb << 16));
+            at<int32_t>(seg_idx, (t * K + k) * 4u) = e;
+            at<float>(seg_score, (t * K + k) * 4u) = sigmoid_fast(__uint_as_float(zb << 16));
             if (load) atomicAdd(&sh_load[e], 1u);
           } else {
             tk = __uint_as_float(zb << 16) + sh_b[e];
@@ -363,14 +401,14 @@ __global__ __launch_bounds__(kBlock) void route_fast_kernel(
         if (k < K) {
           const uint2 v = myrank[k];
           const int e = (int)(v.y & 0xFF);
-          topk_idx[t * K + k] = e;
-          topk_score[t * K + k] = sigmoid_fast(__uint_as_float((v.y >> 16) << 16));
+          at<int32_t>(seg_idx, (t * K + k) * 4u) = e;
+          at<float>(seg_score, (t * K + k) * 4u) = sigmoid_fast(__uint_as_float((v.y >> 16) << 16));
           if (load) atomicAdd(&sh_load[e], 1u);
         }
       }
       tv = __uint_as_float(myrank[K].x);
     }
-    if (valid && g == 0) tau[t] = tv;
+    if (valid && g == 0) at<float>(seg_tau, t * 4u) = tv;
 
     // ---- coarse counts: raw high byte of bf16(tau - z), two margins per conversion
     if (hist && valid) {
@@ -390,23 +428,31 @@ __global__ __launch_bounds__(kBlock) void route_fast_kernel(
 
   for_each_segment(r0, r1, pt, [&](int p, int64_t s0, int64_t s1) {
     uint2 bufa[NQ], bufb[NQ];
-    auto load_rows = [&](uint2* dst, int64_t base) {
-      const int64_t t = base + wave * R + r;
+    // a row past the segment reads the segment's last row; it is processed
+    // as invalid (no output, no count)
+    seg_z = z + s0 * E;
+    seg_idx = topk_idx + s0 * K;
+    seg_score = topk_score + s0 * K;
+    seg_tau = tau + s0;
+    const uint32_t n = (uint32_t)(s1 - s0);
+    auto load_rows = [&](uint2* dst, uint32_t base) {
+      uint32_t t = base + wave * R + r;
+      t = t < n ? t : n - 1;
+      const uint32_t off = (t * (uint32_t)E + (uint32_t)g * 4u) * 2u;    // bytes, < 2^25
 #pragma unroll
-      for (int q = 0; q < NQ; ++q) dst[q] = make_uint2(0, 0);
-      if (t < s1) {
-        const uint2* row = reinterpret_cast<const uint2*>(z + t * E);
-#pragma unroll
-        for (int q = 0; q < NQ; ++q) dst[q] = row[ex(q) >> 2];
-      }
+      for (int q = 0; q < NQ; ++q) dst[q] = at<uint2>(seg_z, off + (uint32_t)q * (8u * G));
     };
-    // the next step's loads are in flight while a step is processed
-    load_rows(bufa, s0);
-    for (int64_t base = s0; base < s1; base += ROWS) {
-      if (base + ROWS < s1) load_rows(bufb, base + ROWS);
-      process(bufa, base + wave * R + r, base + wave * R + r < s1);
+    // The next step's loads are in flight while a step is processed.  Each
+    // step starts by taking the rows prefetched one step earlier, so no load
+    // is still pending in the registers a step works on and the only wait is
+    // for loads issued a whole step before.
+    load_rows(bufb, 0);
+    for (uint32_t base = 0; base < n; base += ROWS) {
 #pragma unroll
       for (int q = 0; q < NQ; ++q) bufa[q] = bufb[q];
+      if (base + ROWS < n) load_rows(bufb, base + ROWS);
+      const uint32_t t = base + wave * R + r;
+      process(bufa, t, t < n);
     }
     __syncthreads();
     if (hist) flush_hist<E, false>(sh_hist, hist + (int64_t)p * E * kNBins, nullptr);
