@@ -188,6 +188,8 @@ def main():
                     help="tokens in the CPU-oracle baseline slice (0 disables it)")
     ap.add_argument("--qb-steps", type=int, default=4,
                     help="steps of the closed QB loop over fresh batches (0 disables it)")
+    ap.add_argument("--no-legs", action="store_true",
+                    help="skip the LEI and comparison-variant legs (for counter collection)")
     ap.add_argument("--stages", action="store_true", help="also print per-stage times to stderr")
     ap.add_argument("--print-source-hash", action="store_true", help="print the kernel source hash and exit")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
@@ -292,8 +294,9 @@ def main():
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": route_gbs / HBM_PEAK_GBS,
                      "traffic": traffic, "algorithmic_bytes": route_bytes},
     }
-    out["lei"] = lei_leg(w, eqb, torch, lay, part_off, stream)
-    out["variants"] = variants_leg(w, eqb, torch, zt, bt, lay, part_off)
+    if not args.no_legs:
+        out["lei"] = lei_leg(w, eqb, torch, lay, part_off, stream)
+        out["variants"] = variants_leg(w, eqb, torch, zt, bt, lay, part_off)
     if args.qb_steps > 0:
         del zt
         out["qb_loop"] = qb_loop_leg(w, eqb, torch, args.qb_steps, dev, part_off)
