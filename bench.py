@@ -117,10 +117,12 @@ def qb_loop_leg(w, eqb, torch, steps, dev, part_off):
             "dev_status": max(r["dev_status"] for r in res)}
 
 
-def lei_leg(w, eqb, torch, lay, part_off, stream, reps=10):
+def lei_leg(w, eqb, torch, lay, zt, part_off, stream, reps=10):
     """Load-Error Injection (Sec. 4) after the step: the residual from the
-    step's per-partition loads and the injection into a [T,E] binary32
-    score-gradient buffer (read and written once: 8 bytes per score)."""
+    step's per-partition loads, the injection into a [T,E] binary32
+    score-gradient buffer (read and written once: 8 bytes per score), and the
+    fused router backward (reads z and the [T,K] mixture gradients, writes the
+    binary32 logit gradient: 6E + 8K bytes per token)."""
     dev = lay.load.device
     inj = torch.empty((w.P, w.E), dtype=torch.float32, device=dev)
     grad = torch.zeros((w.T, w.E), dtype=torch.float32, device=dev)
@@ -139,10 +141,24 @@ def lei_leg(w, eqb, torch, lay, part_off, stream, reps=10):
     torch.cuda.synchronize()
     inject_ms = ev[1].elapsed_time(ev[2]) / reps
     gbs = 8.0 * w.T * w.E / (inject_ms * 1e-3) / 1e9
-    del grad
+    # fused router backward: the step's scores stand in for the mixture gradients
+    gz = grad
+    bw = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    with torch.cuda.stream(stream):
+        eqb.eqb_lei_router_backward(zt, lay.topk_idx, lay.topk_score, gz, inj, part_off, stream)
+        bw[0].record(stream)
+        for _ in range(reps):
+            eqb.eqb_lei_router_backward(zt, lay.topk_idx, lay.topk_score, gz, inj, part_off, stream)
+        bw[1].record(stream)
+    torch.cuda.synchronize()
+    bwd_ms = bw[0].elapsed_time(bw[1]) / reps
+    bwd_bytes = (6 * w.E + 8 * w.K) * w.T
+    bwd_gbs = bwd_bytes / (bwd_ms * 1e-3) / 1e9
+    del grad, gz
     return {"residual_us": ev[0].elapsed_time(ev[1]) * 1e3 / reps, "inject_ms": inject_ms,
             "inject_bytes": 8 * w.T * w.E, "inject_gbs": gbs, "inject_frac_of_peak": gbs / HBM_PEAK_GBS,
-            "eta": 2e-5, "c": 1.0}
+            "router_backward_ms": bwd_ms, "router_backward_bytes": bwd_bytes, "router_backward_gbs": bwd_gbs,
+            "router_backward_frac_of_peak": bwd_gbs / HBM_PEAK_GBS, "eta": 2e-5, "c": 1.0}
 
 
 def variants_leg(w, eqb, torch, zt, bt, lay, part_off):
@@ -295,7 +311,7 @@ def main():
                      "traffic": traffic, "algorithmic_bytes": route_bytes},
     }
     if not args.no_legs:
-        out["lei"] = lei_leg(w, eqb, torch, lay, part_off, stream)
+        out["lei"] = lei_leg(w, eqb, torch, lay, zt, part_off, stream)
         out["variants"] = variants_leg(w, eqb, torch, zt, bt, lay, part_off)
     if args.qb_steps > 0:
         del zt

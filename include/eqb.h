@@ -220,6 +220,22 @@ eqb_status eqb_lei_residual(const int32_t* load, int64_t T, int32_t K, int32_t E
 eqb_status eqb_lei_inject(float* grad_s, const float* inj, int64_t T, int32_t E,
                           const int64_t* part_off, int32_t P, void* stream);
 
+/*
+ * Router backward with Load-Error Injection, fused (Sec. 2 Eq. 1; Sec. 4 Eq. lei):
+ *   grad_z[t,e] = (g[t,e] + inj[p,e]) * sigmoid'(z[t,e])    for t in partition p,
+ *   where g[t,e] = grad_score[t,k] if e = topk_idx[t,k] (the gradient of the
+ *   loss w.r.t. the mixture weight s_{t,e} of a selected expert) and 0 for the
+ *   other experts; inj [P,E] from eqb_lei_residual, or NULL for the plain
+ *   router backward.  sigmoid'(z) = e/(1+e)^2, e = exp(-|z|), in binary32
+ *   (a few ulp); the sum and product are single binary32 operations.
+ *   z [T,E] bf16 bits (16-byte aligned), topk_idx [T,K] int32, grad_score
+ *   [T,K] binary32 (in); grad_z [T,E] binary32 (out, 16-byte aligned).
+ *   Index entries outside [0, E) are ignored.
+ */
+eqb_status eqb_lei_router_backward(const uint16_t* z, const int32_t* topk_idx, const float* grad_score,
+                                   const float* inj, int64_t T, int32_t E, int32_t K, const int64_t* part_off,
+                                   int32_t P, float* grad_z, void* stream);
+
 /* Host helper: r = ceil(T*K/E) (Sec. 3; the paper assumes T*K/E is an
  * integer), or -1 for invalid arguments.  Host only, no HIP call. */
 int64_t eqb_rank(int64_t T_total, int32_t K, int32_t E);

@@ -18,6 +18,12 @@ Written from arXiv 2609.28053:
   rho~ = rho tanh(xi)/xi with xi = ||rho||_inf / c (and tanh(xi)/xi := 1 at
   xi = 0); the router-score gradient of every token of that local batch gets
   grad_{s_{t,e}} += eta rho~_e.
+* The router backward with LEI (Sec. 2 Eq. 1; Sec. 4 Eq. lei): with
+  s_{t,e} = sigmoid(z_{t,e}) weighting the selected experts, the gradient of
+  the loss w.r.t. the logits is (g_{t,e} + eta rho~_{p(t),e}) * s (1 - s),
+  where g_{t,e} is the mixture-weight gradient of a selected expert (zero for
+  the others) and the injected term reaches every expert of every token of
+  the local batch.
 * The two distributed QB statistics EQB is compared with (Sec. 2, after
   Eq. 2; Sec. 3): the rank-averaged quantile, where each rank takes the K/E
   quantile of its own shard and the ranks average them, and the
@@ -37,6 +43,10 @@ Readings taken where the paper is silent:
     unnormalised form (rho~ = rho).  An empty local batch injects 0.
   * The injection itself is one binary32 addition per score, rounded to
     nearest even.
+  * Router backward: sigmoid'(z) = e / (1 + e)^2 with e = exp(-|z|), in
+    binary64; the selected experts' gradients arrive as [T,K] with their
+    indices; the result is compared with the device's binary32 within a
+    tolerance (the device evaluates exp in binary32).
   * Rank-averaged QB: shard p's quantile is its exact r_p-th smallest BF16
     margin, r_p = ceil(|B_p| K/E); the average over the non-empty shards is a
     binary64 sum in ascending p divided by their number; the result is
@@ -134,6 +144,23 @@ def lei_inject(grad_s, inj, part_off) -> np.ndarray:
         r0, r1 = int(part_off[p]), int(part_off[p + 1])
         out[r0:r1] = (grad_s[r0:r1] + inj[p][None, :]).astype(np.float32)
     return out
+
+
+def lei_router_backward(z_bits, topk_idx, grad_score, inj, part_off) -> np.ndarray:
+    """d loss / d z [T,E] in binary64: (g_{t,e} + inj[p(t),e]) * sigmoid'(z_{t,e}),
+    g_{t,e} the mixture-weight gradient of selected experts (from [T,K]); inj
+    may be None (no injection)."""
+    zf = _eqb.bf16_to_f32(z_bits).astype(np.float64)
+    T, E = zf.shape
+    part_off = np.asarray(part_off, np.int64)
+    g = np.zeros((T, E), np.float64)
+    rows = np.repeat(np.arange(T), np.asarray(topk_idx).shape[1])
+    g[rows, np.asarray(topk_idx).ravel()] = np.asarray(grad_score, np.float32).astype(np.float64).ravel()
+    if inj is not None:
+        for p in range(part_off.size - 1):
+            g[part_off[p]:part_off[p + 1]] += np.asarray(inj[p], np.float32).astype(np.float64)[None, :]
+    e = np.exp(-np.abs(zf))
+    return g * (e / (1.0 + e) ** 2)
 
 
 # --------------------------------------------------------------------------

@@ -113,6 +113,89 @@ __global__ __launch_bounds__(kBlock) void lei_inject_kernel(
   });
 }
 
+// ------------------------------------- router backward with LEI ---------
+// grad_z[t,e] = (g[t,e] + inj[p(t),e]) * sigmoid'(z[t,e]), where g[t,e] is
+// grad_score[t,k] for e = topk_idx[t,k] and 0 for the other experts.  G = E/8
+// lanes hold a row, 8 experts each (one 16-byte load of z, two of grad_z).
+// The K mixture gradients of a row are scattered into a per-wave LDS row
+// (zeroed first) and read back 8 at a time.
+template <int E>
+__global__ __launch_bounds__(kBlock) void lei_router_backward_kernel(
+    const uint16_t* __restrict__ z, const int32_t* __restrict__ topk_idx, const float* __restrict__ grad_score,
+    const float* __restrict__ inj, int64_t T, int K, float* __restrict__ grad_z, const PartTable pt,
+    int64_t rows_per_block) {
+  constexpr int G = E / 8;
+  constexpr int R = 64 / G;
+  constexpr int ROWS = kWaves * R;
+  __shared__ __align__(16) float sh_g[kWaves][R][E];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int g = lane % G, rr = lane / G;
+  const int e0 = g * 8;
+  float* myrow = sh_g[wave][rr];
+  int64_t r0, r1;
+  block_rows(T, rows_per_block, &r0, &r1);
+  for_each_segment(r0, r1, pt, [&](int p, int64_t s0, int64_t s1) {
+    float d[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) d[j] = inj ? inj[(int64_t)p * E + e0 + j] : 0.0f;
+    for (int64_t base = s0; base < s1; base += ROWS) {
+      const int64_t t = base + wave * R + rr;
+      const bool valid = t < s1;
+      uint4 zw = make_uint4(0, 0, 0, 0);
+      if (valid) zw = *reinterpret_cast<const uint4*>(z + t * E + e0);
+      // scatter the row's mixture gradients
+      *reinterpret_cast<float4*>(myrow + e0) = make_float4(0.f, 0.f, 0.f, 0.f);
+      *reinterpret_cast<float4*>(myrow + e0 + 4) = make_float4(0.f, 0.f, 0.f, 0.f);
+      lds_wave_sync();
+      if (valid) {
+        for (int k = g; k < K; k += G) {
+          const int e = topk_idx[t * K + k];
+          if (e >= 0 && e < E) myrow[e] = grad_score[t * K + k];
+        }
+      }
+      lds_wave_sync();
+      const float4 ga = *reinterpret_cast<const float4*>(myrow + e0);
+      const float4 gb = *reinterpret_cast<const float4*>(myrow + e0 + 4);
+      const float gm[8] = {ga.x, ga.y, ga.z, ga.w, gb.x, gb.y, gb.z, gb.w};
+      const uint32_t w4[4] = {zw.x, zw.y, zw.z, zw.w};
+      float o[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const float zf = (j & 1) ? bf16_hi(w4[j >> 1]) : bf16_lo(w4[j >> 1]);
+        o[j] = (gm[j] + d[j]) * sigmoid_prime_fast(zf);
+      }
+      if (valid) {
+        *reinterpret_cast<float4*>(grad_z + t * E + e0) = make_float4(o[0], o[1], o[2], o[3]);
+        *reinterpret_cast<float4*>(grad_z + t * E + e0 + 4) = make_float4(o[4], o[5], o[6], o[7]);
+      }
+      lds_wave_sync();          // the row buffer is rewritten by the next step
+    }
+  });
+}
+
+template <int E>
+static void launch_backward_e(const uint16_t* z, const int32_t* idx, const float* gs, const float* inj, int64_t T,
+                              int K, float* gz, const PartTable& pt, hipStream_t s) {
+  int blocks;
+  int64_t rpb;
+  grid_for(T, kWaves * (64 / (E / 8)), 2, &blocks, &rpb);
+  lei_router_backward_kernel<E><<<blocks, kBlock, 0, s>>>(z, idx, gs, inj, T, K, gz, pt, rpb);
+}
+
+eqb_status launch_lei_router_backward(const uint16_t* z, const int32_t* idx, const float* gs, const float* inj,
+                                      int64_t T, int E, int K, float* gz, const PartTable& pt, hipStream_t s) {
+  switch (E) {
+    case 8: launch_backward_e<8>(z, idx, gs, inj, T, K, gz, pt, s); break;
+    case 16: launch_backward_e<16>(z, idx, gs, inj, T, K, gz, pt, s); break;
+    case 32: launch_backward_e<32>(z, idx, gs, inj, T, K, gz, pt, s); break;
+    case 64: launch_backward_e<64>(z, idx, gs, inj, T, K, gz, pt, s); break;
+    case 128: launch_backward_e<128>(z, idx, gs, inj, T, K, gz, pt, s); break;
+    case 256: launch_backward_e<256>(z, idx, gs, inj, T, K, gz, pt, s); break;
+    default: return EQB_ERR_UNSUPPORTED;
+  }
+  return launch_status();
+}
+
 eqb_status launch_lei_residual(const int32_t* load, int E, int K, const PartTable& pt, double eta,
                                double c, float* inj, hipStream_t s) {
   lei_residual_kernel<<<pt.P, kNBins, 0, s>>>(load, E, K, pt, eta, c, inj);

@@ -248,6 +248,21 @@ eqb_status eqb_lei_inject(float* grad_s, const float* inj, int64_t T, int32_t E,
   return launch_lei_inject(grad_s, inj, T, E, pt, static_cast<hipStream_t>(stream));
 }
 
+eqb_status eqb_lei_router_backward(const uint16_t* z, const int32_t* topk_idx, const float* grad_score,
+                                   const float* inj, int64_t T, int32_t E, int32_t K, const int64_t* part_off,
+                                   int32_t P, float* grad_z, void* stream) {
+  if (T < 0 || T > INT32_MAX || K < 1 || K >= E) return EQB_ERR_INVALID_ARG;
+  if (!supported_E(E)) return EQB_ERR_UNSUPPORTED;
+  PartTable pt;
+  const eqb_status st = make_table(part_off, P, T, &pt);
+  if (st != EQB_OK) return st;
+  if (T == 0) return EQB_OK;
+  if (!z || !topk_idx || !grad_score || !grad_z) return EQB_ERR_INVALID_ARG;
+  if (!aligned16(z) || !aligned16(grad_z)) return EQB_ERR_UNSUPPORTED;
+  return launch_lei_router_backward(z, topk_idx, grad_score, inj, T, E, K, grad_z, pt,
+                                    static_cast<hipStream_t>(stream));
+}
+
 int64_t eqb_rank(int64_t T_total, int32_t K, int32_t E) {
   if (T_total < 0 || E < 1 || K < 1 || K >= E) return -1;
   if (T_total > ((int64_t)1 << 40)) return -1;

@@ -69,6 +69,27 @@ __device__ __forceinline__ float sigmoid_fast(float x) {
   return x >= 0.0f ? r : e * r;
 }
 
+// sigmoid'(x) = e / (1 + e)^2 with e = exp(-|x|) (the form that keeps its
+// relative accuracy for large |x|), e from the same split base-2 exponential
+// as sigmoid_fast; a few ulp for |x| <= 64, the libm exponential beyond.
+__device__ __forceinline__ float sigmoid_prime_fast(float x) {
+  const float a = fabsf(x);
+  float e;
+  if (a > 64.0f) {
+    e = expf(-a);
+  } else {
+    const float kLog2eHi = 1.44269502162933349609375f;
+    const float kLog2eLo = 1.925963033500011e-08f;
+    const float kLn2 = 0.693147180559945309f;
+    const float p_hi = a * kLog2eHi;
+    const float p_lo = __builtin_fmaf(a, kLog2eLo, __builtin_fmaf(a, kLog2eHi, -p_hi));
+    const float e1 = __builtin_amdgcn_exp2f(-p_hi);
+    e = __builtin_fmaf(-e1, p_lo * kLn2, e1);
+  }
+  const float r = 1.0f / (1.0f + e);
+  return e * r * r;
+}
+
 // ------------------------------------------------------- exact 64-bit keys --
 // Unsigned key ordered like the binary32 value, with -0 and +0 equal.
 __device__ __forceinline__ uint32_t order_key(uint32_t u) {

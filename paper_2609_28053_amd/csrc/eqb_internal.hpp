@@ -51,6 +51,8 @@ eqb_status launch_max_violation(const int32_t* load, int E, int K, const PartTab
 
 eqb_status launch_lei_residual(const int32_t* load, int E, int K, const PartTable& pt, double eta,
                                double c, float* inj, hipStream_t s);
+eqb_status launch_lei_router_backward(const uint16_t* z, const int32_t* idx, const float* gs, const float* inj,
+                                      int64_t T, int E, int K, float* gz, const PartTable& pt, hipStream_t s);
 eqb_status launch_lei_inject(float* grad, const float* inj, int64_t T, int E, const PartTable& pt,
                              hipStream_t s);
 

@@ -42,6 +42,7 @@ EXPORTS = (
     "eqb_max_violation",
     "eqb_lei_residual",
     "eqb_lei_inject",
+    "eqb_lei_router_backward",
     "eqb_rank",
     "eqb_status_string",
 )
@@ -70,6 +71,7 @@ def _load():
         "eqb_max_violation": [P, i64, i32, i32, P, i32, P, P, P],
         "eqb_lei_residual": [P, i64, i32, i32, P, i32, ctypes.c_double, ctypes.c_double, P, P],
         "eqb_lei_inject": [P, P, i64, i32, P, i32, P],
+        "eqb_lei_router_backward": [P, P, P, P, i64, i32, i32, P, i32, P, P],
         "eqb_rank": [i64, i32, i32],
         "eqb_status_string": [i32],
     }
@@ -267,6 +269,17 @@ def eqb_lei_inject(grad_s, inj, part_off=None, stream=None):
     _check("eqb_lei_inject", lib.eqb_lei_inject(
         _ptr(grad_s, torch.float32, T * E, "grad_s"), _ptr(inj, torch.float32, P * E, "inj"), T, E,
         po, P, _stream(stream)))
+    del keep
+
+
+def eqb_lei_router_backward(z, topk_idx, grad_score, grad_z, inj=None, part_off=None, stream=None):
+    T, E = z.shape
+    K = topk_idx.shape[1]
+    po, P, keep = _offsets(part_off, T)
+    _check("eqb_lei_router_backward", lib.eqb_lei_router_backward(
+        _ptr(z, _Z, name="z"), _ptr(topk_idx, torch.int32, T * K, "topk_idx"),
+        _ptr(grad_score, torch.float32, T * K, "grad_score"), _ptr(inj, torch.float32, P * E, "inj"),
+        T, E, K, po, P, _ptr(grad_z, torch.float32, T * E, "grad_z"), _stream(stream)))
     del keep
 
 

@@ -33,6 +33,7 @@ def lib():
     lib.eqb_max_violation.argtypes = [V, i64, i32, i32, V, i32, V, V, V]
     lib.eqb_lei_residual.argtypes = [V, i64, i32, i32, V, i32, ctypes.c_double, ctypes.c_double, V, V]
     lib.eqb_lei_inject.argtypes = [V, V, i64, i32, V, i32, V]
+    lib.eqb_lei_router_backward.argtypes = [V, V, V, V, i64, i32, i32, V, i32, V, V]
     lib.eqb_rank.argtypes = [i64, i32, i32]
     lib.eqb_rank.restype = i64
     lib.eqb_status_string.argtypes = [i32]
@@ -154,6 +155,17 @@ def test_lei_checks(lib):
     po, keep = offs(0, 10, 63)
     assert i(FAKE, FAKE, 64, 8, po, 2, None) == INVALID
     assert i(FAKE, FAKE, 0, 8, None, 1, None) == OK
+
+
+def test_router_backward_checks(lib):
+    f = lib.eqb_lei_router_backward
+    assert f(None, FAKE, FAKE, None, 64, 8, 2, None, 1, FAKE, None) == INVALID
+    assert f(FAKE, FAKE, FAKE, None, 64, 8, 2, None, 1, None, None) == INVALID
+    assert f(FAKE, FAKE, FAKE, None, 64, 8, 8, None, 1, FAKE, None) == INVALID      # K >= E
+    assert f(FAKE, FAKE, FAKE, None, 64, 24, 2, None, 1, FAKE, None) == UNSUPPORTED
+    assert f(ctypes.c_void_p(0x10002), FAKE, FAKE, None, 64, 8, 2, None, 1, FAKE, None) == UNSUPPORTED
+    assert f(FAKE, FAKE, FAKE, None, 64, 8, 2, None, 1, ctypes.c_void_p(0x10004), None) == UNSUPPORTED
+    assert f(FAKE, FAKE, FAKE, None, 0, 8, 2, None, 1, FAKE, None) == OK
 
 
 def test_rank_and_status_strings(lib):

@@ -337,3 +337,32 @@ def test_variant_pins_catch_planted_mistakes(monkeypatch, mutant):
         except AssertionError:
             failed = True
     assert failed, mutant
+
+
+# ------------------------------------------------ router backward with LEI ---
+def test_router_backward_is_the_autograd_gradient():
+    """Eq. 1 and Eq. lei: the logits' gradient of sum_{t,k} g_{t,k} s_{t,idx} plus
+    the injected sum_{t,e} inj_{p(t),e} s_{t,e}, by torch autograd in float64."""
+    import torch
+    rng = np.random.default_rng(4)
+    T, E, K = 40, 16, 3
+    z = O.f32_to_bf16_rne((rng.standard_normal((T, E)) * 3).astype(np.float32))
+    idx = np.stack([rng.choice(E, K, replace=False) for _ in range(T)]).astype(np.int32)
+    gs = rng.standard_normal((T, K)).astype(np.float32)
+    off = np.array([0, 15, 15, 40])
+    inj = (rng.standard_normal((3, E)) * 1e-2).astype(np.float32)
+    zt = torch.tensor(O.bf16_to_f32(z).astype(np.float64), requires_grad=True)
+    s = torch.sigmoid(zt)
+    loss = (torch.tensor(gs, dtype=torch.float64) * s.gather(1, torch.tensor(idx, dtype=torch.int64))).sum()
+    pid = np.searchsorted(off, np.arange(T), side="right") - 1
+    loss = loss + (torch.tensor(inj.astype(np.float64)[pid]) * s).sum()
+    loss.backward()
+    got = B.lei_router_backward(z, idx, gs, inj, off)
+    np.testing.assert_allclose(got, zt.grad.numpy(), rtol=1e-12, atol=1e-300)
+    # without injection only the selected experts move
+    plain = B.lei_router_backward(z, idx, gs, None, off)
+    mask = np.zeros((T, E), bool)
+    mask[np.repeat(np.arange(T), K), idx.ravel()] = True
+    assert np.all(plain[~mask] == 0)
+    assert B.lei_router_backward(np.zeros((1, 2), np.uint16), np.array([[0]]), np.array([[1.0]], np.float32),
+                                 None, [0, 1])[0, 0] == 0.25          # sigmoid'(0) = 1/4

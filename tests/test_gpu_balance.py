@@ -146,3 +146,34 @@ def test_lei_on_a_routed_layer(eqb):
     gg = grad.cpu().numpy()
     for p in range(w.P):
         np.testing.assert_array_equal(gg[off[p]:off[p + 1]], np.broadcast_to(got_inj[p], (off[p + 1] - off[p], w.E)))
+
+
+# ------------------------------------------------ router backward with LEI ---
+@pytest.mark.parametrize("E,K,T,P,with_inj", [(8, 2, 1001, 1, True), (64, 6, 20011, 4, True),
+                                              (256, 8, 70001, 16, True), (256, 8, 9000, 1, False),
+                                              (128, 14, 5003, 8, True)])
+def test_lei_router_backward_matches_oracle(eqb, E, K, T, P, with_inj):
+    """The device evaluates sigmoid' in binary32 (split base-2 exponential,
+    reciprocal, two products) and the sum and product once each: a few ulp of
+    the result, bounded here by 2e-6 relative; results that underflow into
+    binary32 subnormals are compared absolutely."""
+    from oracle import eqb_oracle as O
+    rng = np.random.default_rng(E * 7 + K)
+    x = rng.standard_normal((T, E)) * 3
+    x[rng.random((T, E)) < 0.01] *= 40                      # a few logits far in the tails
+    z = O.f32_to_bf16_rne(x.astype(np.float32))
+    idx = np.argsort(rng.random((T, E)), axis=1)[:, :K].astype(np.int32)
+    gs = rng.standard_normal((T, K)).astype(np.float32)
+    off = np.linspace(0, T, P + 1).astype(np.int64)
+    if P > 2:
+        off[2] = off[1]
+    inj = (rng.standard_normal((P, E)) * 1e-3).astype(np.float32) if with_inj else None
+    say(f"router backward E={E} K={K} T={T} P={P} inj={with_inj}")
+    gz = torch.empty((T, E), dtype=torch.float32, device="cuda")
+    eqb.eqb_lei_router_backward(torch.from_numpy(z.view(np.int16)).cuda(), torch.from_numpy(idx).cuda(),
+                                torch.from_numpy(gs).cuda(), gz,
+                                None if inj is None else torch.from_numpy(inj).cuda(), [int(v) for v in off])
+    got = gz.cpu().numpy().astype(np.float64)
+    want = B.lei_router_backward(z, idx, gs, inj, off)
+    err = np.abs(got - want)
+    assert np.all(err <= 2e-6 * np.abs(want) + 1e-37), float(np.max(err / (np.abs(want) + 1e-300)))
