@@ -236,6 +236,17 @@ eqb_status eqb_lei_router_backward(const uint16_t* z, const int32_t* topk_idx, c
                                    const float* inj, int64_t T, int32_t E, int32_t K, const int64_t* part_off,
                                    int32_t P, float* grad_z, void* stream);
 
+/*
+ * Tuning control (host only, no HIP call): caps the number of blocks of the
+ * streaming kernels (routing, the margin passes, the LEI kernels) at
+ * max_blocks for the calls that follow, in this process; 0 restores the
+ * default (a whole number of blocks per compute unit).  Results do not
+ * depend on it; tests use it to run one block, or a block count that does not
+ * divide the rows, against the same oracle.  Negative values are
+ * EQB_ERR_INVALID_ARG.
+ */
+eqb_status eqb_set_max_blocks(int32_t max_blocks);
+
 /* Host helper: r = ceil(T*K/E) (Sec. 3; the paper assumes T*K/E is an
  * integer), or -1 for invalid arguments.  Host only, no HIP call. */
 int64_t eqb_rank(int64_t T_total, int32_t K, int32_t E);

@@ -1,5 +1,7 @@
 // eqb_api.hip - the C ABI declared in include/eqb.h.  Every argument check
 // runs before anything is enqueued; the calls never synchronise the host.
+#include <atomic>
+
 #include "eqb_internal.hpp"
 
 namespace eqb {
@@ -15,6 +17,12 @@ int num_cus() {
   }
   return cached[dev];
 }
+
+namespace {
+std::atomic<int> g_max_blocks{0};
+}  // namespace
+
+int max_blocks_cap() { return g_max_blocks.load(std::memory_order_relaxed); }
 
 namespace {
 
@@ -261,6 +269,12 @@ eqb_status eqb_lei_router_backward(const uint16_t* z, const int32_t* topk_idx, c
   if (!aligned16(z) || !aligned16(grad_z)) return EQB_ERR_UNSUPPORTED;
   return launch_lei_router_backward(z, topk_idx, grad_score, inj, T, E, K, grad_z, pt,
                                     static_cast<hipStream_t>(stream));
+}
+
+eqb_status eqb_set_max_blocks(int32_t max_blocks) {
+  if (max_blocks < 0) return EQB_ERR_INVALID_ARG;
+  g_max_blocks.store(max_blocks, std::memory_order_relaxed);
+  return EQB_OK;
 }
 
 int64_t eqb_rank(int64_t T_total, int32_t K, int32_t E) {

@@ -59,11 +59,17 @@ eqb_status launch_lei_inject(float* grad, const float* inj, int64_t T, int E, co
 // Number of compute units of the current device (cached per device).
 int num_cus();
 
+// Upper bound on the grid of the streaming kernels set by eqb_set_max_blocks
+// (0: none).
+int max_blocks_cap();
+
 // Blocks and rows per block for a streaming kernel over T rows that advances
 // rows_per_step rows per block step: at most blocks_per_cu blocks per CU,
 // each owning a contiguous range of whole steps.
 inline void grid_for(int64_t T, int rows_per_step, int blocks_per_cu, int* blocks, int64_t* rows_per_block) {
-  const int64_t max_blocks = (int64_t)num_cus() * blocks_per_cu;
+  int64_t max_blocks = (int64_t)num_cus() * blocks_per_cu;
+  const int cap = max_blocks_cap();
+  if (cap > 0 && cap < max_blocks) max_blocks = cap;
   const int64_t steps = (T + rows_per_step - 1) / rows_per_step;
   int64_t nb = steps < max_blocks ? steps : max_blocks;
   if (nb < 1) nb = 1;

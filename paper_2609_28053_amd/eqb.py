@@ -43,6 +43,7 @@ EXPORTS = (
     "eqb_lei_residual",
     "eqb_lei_inject",
     "eqb_lei_router_backward",
+    "eqb_set_max_blocks",
     "eqb_rank",
     "eqb_status_string",
 )
@@ -72,6 +73,7 @@ def _load():
         "eqb_lei_residual": [P, i64, i32, i32, P, i32, ctypes.c_double, ctypes.c_double, P, P],
         "eqb_lei_inject": [P, P, i64, i32, P, i32, P],
         "eqb_lei_router_backward": [P, P, P, P, i64, i32, i32, P, i32, P, P],
+        "eqb_set_max_blocks": [i32],
         "eqb_rank": [i64, i32, i32],
         "eqb_status_string": [i32],
     }
@@ -281,6 +283,10 @@ def eqb_lei_router_backward(z, topk_idx, grad_score, grad_z, inj=None, part_off=
         _ptr(grad_score, torch.float32, T * K, "grad_score"), _ptr(inj, torch.float32, P * E, "inj"),
         T, E, K, po, P, _ptr(grad_z, torch.float32, T * E, "grad_z"), _stream(stream)))
     del keep
+
+
+def eqb_set_max_blocks(max_blocks: int) -> None:
+    _check("eqb_set_max_blocks", lib.eqb_set_max_blocks(int(max_blocks)))
 
 
 def eqb_rank(T_total: int, K: int, E: int) -> int:

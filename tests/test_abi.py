@@ -34,6 +34,7 @@ def lib():
     lib.eqb_lei_residual.argtypes = [V, i64, i32, i32, V, i32, ctypes.c_double, ctypes.c_double, V, V]
     lib.eqb_lei_inject.argtypes = [V, V, i64, i32, V, i32, V]
     lib.eqb_lei_router_backward.argtypes = [V, V, V, V, i64, i32, i32, V, i32, V, V]
+    lib.eqb_set_max_blocks.argtypes = [i32]
     lib.eqb_rank.argtypes = [i64, i32, i32]
     lib.eqb_rank.restype = i64
     lib.eqb_status_string.argtypes = [i32]
@@ -166,6 +167,12 @@ def test_router_backward_checks(lib):
     assert f(ctypes.c_void_p(0x10002), FAKE, FAKE, None, 64, 8, 2, None, 1, FAKE, None) == UNSUPPORTED
     assert f(FAKE, FAKE, FAKE, None, 64, 8, 2, None, 1, ctypes.c_void_p(0x10004), None) == UNSUPPORTED
     assert f(FAKE, FAKE, FAKE, None, 0, 8, 2, None, 1, FAKE, None) == OK
+
+
+def test_set_max_blocks(lib):
+    assert lib.eqb_set_max_blocks(-1) == INVALID
+    assert lib.eqb_set_max_blocks(3) == OK
+    assert lib.eqb_set_max_blocks(0) == OK
 
 
 def test_rank_and_status_strings(lib):

@@ -177,3 +177,25 @@ def test_lei_router_backward_matches_oracle(eqb, E, K, T, P, with_inj):
     want = B.lei_router_backward(z, idx, gs, inj, off)
     err = np.abs(got - want)
     assert np.all(err <= 2e-6 * np.abs(want) + 1e-37), float(np.max(err / (np.abs(want) + 1e-300)))
+
+
+@pytest.mark.parametrize("cap", [1, 5])
+def test_lei_and_variants_under_forced_grid_shapes(eqb, cap):
+    from paper_2609_28053_amd import eqb as binding
+    try:
+        binding.eqb_set_max_blocks(cap)
+        say(f"grid cap {cap}: lei and variants")
+        test_lei_inject_matches_oracle(eqb, 64, 20011, 5)
+        test_lei_router_backward_matches_oracle(eqb, 256, 8, 9000, 4, True)
+        w = W.CONFIGS["skew64"].with_T(20011, 4)
+        z, b, off = W.generate(w)
+        want_bp, want_avg, want_b = B.rank_averaged_qb(z, b, w.K, off)
+        got = eqb.rank_averaged_qb(torch.from_numpy(z.view(np.int16)).cuda(), torch.from_numpy(b).cuda(), w.K,
+                                   [int(x) for x in off])
+        np.testing.assert_array_equal(got["bhat_p"], want_bp)
+        want_c, want_est, _ = B.histogram_qb(z, b, w.K, off, -8.0, 8.0, 100)
+        got = eqb.histogram_qb(torch.from_numpy(z.view(np.int16)).cuda(), torch.from_numpy(b).cuda(), w.K,
+                               -8.0, 8.0, 100, [int(x) for x in off])
+        np.testing.assert_array_equal(got["counts"], want_c)
+    finally:
+        binding.eqb_set_max_blocks(0)

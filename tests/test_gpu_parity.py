@@ -286,3 +286,36 @@ def test_device_rounding_exhaustive_through_both_passes(eqb):
                 got = L.cpu().numpy()[0]
                 for j, u in enumerate(group):
                     np.testing.assert_array_equal(got[j], fine[u], err_msg=f"fine chunk {c:#x} u={u:#x}")
+
+
+# ------------------------------------------------- forced grid shapes (T7) --
+@pytest.mark.parametrize("cap", [1, 3, 7])
+def test_forced_grid_shapes(eqb, cap):
+    """One block, or a few blocks whose row ranges do not divide T, must give
+    the oracle's results: catches missing LDS barriers and flush races."""
+    cases = [("skew64", 70001, 4), ("large256", 30011, 16), ("tiny", 5000, 3)]
+    try:
+        eqb.eqb_set_max_blocks(cap)
+        for name, T, P in cases:
+            w, z, b, off = workload(name, T, P)
+            say(f"grid cap {cap}: {name} T={T} P={P}")
+            want = oracle_for(name, T, P)
+            assert_parity(gpu_layer(eqb, z, b, w.K, off, fused=True), want, w.K)
+            assert_parity(gpu_layer(eqb, z, b, w.K, off, fused=False), want, w.K)
+    finally:
+        eqb.eqb_set_max_blocks(0)
+
+
+def test_token_permutation_on_gpu(eqb):
+    """Permuting the tokens of one partition permutes I and tau and leaves
+    the loads and every EQB statistic unchanged."""
+    w, z, b, _ = workload("large256", 20000, 16)
+    perm = np.random.default_rng(9).permutation(w.T)
+    say("token permutation")
+    a = gpu_layer(eqb, z, b, w.K, None)
+    c = gpu_layer(eqb, np.ascontiguousarray(z[perm]), b, w.K, None)
+    np.testing.assert_array_equal(c["idx"], a["idx"][perm])
+    np.testing.assert_array_equal(c["tau"].view(np.uint32), a["tau"][perm].view(np.uint32))
+    for k in ("load", "H", "L", "u", "v", "rho", "bhat"):
+        np.testing.assert_array_equal(c[k], a[k])
+    np.testing.assert_array_equal(c["b_next"].view(np.uint32), a["b_next"].view(np.uint32))
