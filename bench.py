@@ -227,7 +227,7 @@ def main():
     from paper_2609_28053_amd import eqb
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
-    w = W.CONFIGS[args.workload]
+    w = W.WORKLOADS[args.workload]
     t0 = time.time()
     z, b, off = W.generate(w)
     print(f"[bench] generated {w.name} T={w.T} E={w.E} K={w.K} P={w.P} in {time.time() - t0:.1f}s",

@@ -75,7 +75,7 @@ def test_local_maxvio_uses_the_partition_size():
 
 def test_qb_loop_balances_fresh_batches():
     """Eq. 2's purpose: the bias from step q balances step q+1's batch."""
-    w = W.CONFIGS["skew64"].with_T(32768, 4)
+    w = W.WORKLOADS["skew64"].with_T(32768, 4)
     batches = [W.generate(w, batch=q)[0] for q in range(4)]
     _, _, off = W.generate(w)
     steps = B.qb_loop(batches, np.zeros(w.E, np.float32), w.K, off)
@@ -229,7 +229,7 @@ from oracle import eqb_oracle as O
 
 
 def test_rank_average_of_one_shard_is_eqb():
-    w = W.CONFIGS["skew64"].with_T(6000, 1)
+    w = W.WORKLOADS["skew64"].with_T(6000, 1)
     z, b, off = W.generate(w)
     bp, avg, bn = B.rank_averaged_qb(z, b, w.K, off)
     ex = O.run_layer(z, b, w.K, off)
@@ -239,7 +239,7 @@ def test_rank_average_of_one_shard_is_eqb():
 
 def test_rank_average_of_identical_shards_is_eqb():
     """P copies of one batch: every shard's quantile is the global one."""
-    w = W.CONFIGS["skew64"].with_T(2048, 1)        # 2048 * 6 / 64 is an integer
+    w = W.WORKLOADS["skew64"].with_T(2048, 1)        # 2048 * 6 / 64 is an integer
     z, b, _ = W.generate(w)
     zz = np.concatenate([z] * 3)
     off = np.array([0, 2048, 4096, 6144])
@@ -251,7 +251,7 @@ def test_rank_average_of_identical_shards_is_eqb():
 
 
 def test_shard_quantile_is_numpys_inverted_cdf_and_average_depends_on_the_split():
-    w = W.CONFIGS["skew64"].with_T(9000, 3)
+    w = W.WORKLOADS["skew64"].with_T(9000, 3)
     z, b, off = W.generate(w)
     bp, avg, _ = B.rank_averaged_qb(z, b, w.K, off)
     _, _, tau = O.route_topk(z, b, w.K)
@@ -267,7 +267,7 @@ def test_shard_quantile_is_numpys_inverted_cdf_and_average_depends_on_the_split(
 
 
 def test_rank_average_skips_empty_shards():
-    w = W.CONFIGS["skew64"].with_T(4000, 2)
+    w = W.WORKLOADS["skew64"].with_T(4000, 2)
     z, b, _ = W.generate(w)
     bp, avg, _ = B.rank_averaged_qb(z, b, w.K, [0, 2000, 2000, 4000])
     assert np.all(bp[1] == 0x7FC0)
@@ -291,7 +291,7 @@ def test_uniform_bins_against_exact_rationals():
 
 
 def test_histogram_estimate_lies_in_the_bin_of_the_exact_quantile():
-    w = W.CONFIGS["skew64"].with_T(9000, 3)
+    w = W.WORKLOADS["skew64"].with_T(9000, 3)
     z, b, off = W.generate(w)
     lo, hi, nb = -10.0, 10.0, 200
     counts, est, bn = B.histogram_qb(z, b, w.K, off, lo, hi, nb)

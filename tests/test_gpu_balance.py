@@ -66,7 +66,7 @@ def check_loop(got, want):
 @pytest.mark.parametrize("name,T,P,steps", [("skew64", 20011, 4, 3), ("large256", 9001, 16, 2),
                                             ("skew64", 262144, 4, 3)])
 def test_qb_loop_matches_oracle(eqb, name, T, P, steps):
-    w = W.CONFIGS[name].with_T(T, P)
+    w = W.WORKLOADS[name].with_T(T, P)
     _, b0, off = W.generate(w)
     batches = [W.generate(w, batch=q)[0] for q in range(steps)]
     say(f"qb loop {name} T={T} P={P} steps={steps}")
@@ -130,7 +130,7 @@ def test_lei_inject_matches_oracle(eqb, E, T, P):
 def test_lei_on_a_routed_layer(eqb):
     """Loads from the routing kernel feed the residual; the injection moves
     only the score gradients, by each partition's value."""
-    w = W.CONFIGS["large256"].with_T(65536, 16)
+    w = W.WORKLOADS["large256"].with_T(65536, 16)
     z, b, off = W.generate(w)
     offl = [int(x) for x in off]
     say("lei on a routed layer")
@@ -187,7 +187,7 @@ def test_lei_and_variants_under_forced_grid_shapes(eqb, cap):
         say(f"grid cap {cap}: lei and variants")
         test_lei_inject_matches_oracle(eqb, 64, 20011, 5)
         test_lei_router_backward_matches_oracle(eqb, 256, 8, 9000, 4, True)
-        w = W.CONFIGS["skew64"].with_T(20011, 4)
+        w = W.WORKLOADS["skew64"].with_T(20011, 4)
         z, b, off = W.generate(w)
         want_bp, want_avg, want_b = B.rank_averaged_qb(z, b, w.K, off)
         got = eqb.rank_averaged_qb(torch.from_numpy(z.view(np.int16)).cuda(), torch.from_numpy(b).cuda(), w.K,

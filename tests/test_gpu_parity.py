@@ -73,7 +73,7 @@ def assert_parity(got, want, K, check_parts=True):
 
 @functools.lru_cache(maxsize=4)
 def workload(name, T=None, P=None):
-    w = W.CONFIGS[name] if T is None else W.CONFIGS[name].with_T(T, P)
+    w = W.WORKLOADS[name] if T is None else W.WORKLOADS[name].with_T(T, P)
     z, b, off = W.generate(w)
     return w, z, b, off
 
@@ -99,7 +99,7 @@ def test_parity_small(eqb, name, T, P):
 
 
 # ---------------------------------------------------------- full sizes ----
-@pytest.mark.parametrize("name", W.CONFIG_ORDER)
+@pytest.mark.parametrize("name", W.WORKLOAD_ORDER)
 def test_parity_full_size(eqb, name):
     w, z, b, off = workload(name)
     say(f"full {name} T={w.T} E={w.E} K={w.K} P={w.P} oracle threads={_threads()}")

@@ -37,7 +37,7 @@ CASES = [("skew64", 20011, 4, None), ("large256", 9001, 16, None), ("split128", 
 
 @pytest.mark.parametrize("name,T,P,cuts", CASES)
 def test_rank_averaged_qb_matches_oracle(eqb, name, T, P, cuts):
-    w = W.CONFIGS[name].with_T(T, P)
+    w = W.WORKLOADS[name].with_T(T, P)
     z, b, off = W.generate(w)
     if cuts is not None:
         off = np.array(cuts, np.int64)
@@ -57,7 +57,7 @@ def test_rank_averaged_qb_matches_oracle(eqb, name, T, P, cuts):
                                                   ("split128", 30011, 8, -1.0, 1.0, 256),
                                                   ("skew64", 262144, 4, -10.0, 10.0, 200)])
 def test_histogram_qb_matches_oracle(eqb, name, T, P, lo, hi, nbins):
-    w = W.CONFIGS[name].with_T(T, P)
+    w = W.WORKLOADS[name].with_T(T, P)
     z, b, off = W.generate(w)
     say(f"histogram {name} T={T} P={P} [{lo},{hi}) nbins={nbins}")
     want_c, want_est, want_b = B.histogram_qb(z, b, w.K, off, lo, hi, nbins)

@@ -331,7 +331,7 @@ def test_hand_worked_examples(case):
 
 # ----------------------------------------------------------- invariants ---
 def _small(name, T, P=None, seed_split=None):
-    w = W.CONFIGS[name].with_T(T, P)
+    w = W.WORKLOADS[name].with_T(T, P)
     z, b, off = W.generate(w)
     if seed_split is not None:
         rng = np.random.default_rng(seed_split)
@@ -340,7 +340,7 @@ def _small(name, T, P=None, seed_split=None):
     return w, z, b, off
 
 
-@pytest.mark.parametrize("name", W.CONFIG_ORDER)
+@pytest.mark.parametrize("name", W.WORKLOAD_ORDER)
 def test_invariants_on_workload_shapes(name):
     w, z, b, off = _small(name, 3000, seed_split=3)
     R = O.run_layer(z, b, w.K, off)

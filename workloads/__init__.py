@@ -63,7 +63,7 @@ class Workload:
 
 # The five workloads: tiny (E=8), skewed E=64, random split E=128,
 # tie-heavy grid E=64, and the large E=256 layer with boosted tokens.
-CONFIGS = {
+WORKLOADS = {
     "tiny": Workload("tiny", T=4096, E=8, K=2, P=1, seed=0, kind="normal",
                      z_sigma=1.0, off_sigma=0.5, b_sigma=0.1),
     "skew64": Workload("skew64", T=262144, E=64, K=6, P=4, seed=1, kind="normal",
@@ -76,7 +76,7 @@ CONFIGS = {
                          z_sigma=1.0, off_sigma=0.7, b_sigma=0.1,
                          boost_frac=0.05, boost=3.0),
 }
-CONFIG_ORDER = ["tiny", "skew64", "split128", "tie64", "large256"]
+WORKLOAD_ORDER = ["tiny", "skew64", "split128", "tie64", "large256"]
 
 TIE_GRID_STEPS = 16   # values k/4 for k = -16..16: 33 distinct BF16 values in [-4, 4]
 
