@@ -75,8 +75,13 @@ WORKLOADS = {
     "large256": Workload("large256", T=4194304, E=256, K=8, P=16, seed=4, kind="boost",
                          z_sigma=1.0, off_sigma=0.7, b_sigma=0.1,
                          boost_frac=0.05, boost=3.0),
+    # one data-parallel rank's share of the paper's optimizer step: 576 sequences
+    # of 16,384 tokens over 64 ranks, E = 256, K = 6 (Appendix E)
+    "rank256": Workload("rank256", T=147456, E=256, K=6, P=1, seed=5, kind="boost",
+                        z_sigma=1.0, off_sigma=0.7, b_sigma=0.1,
+                        boost_frac=0.05, boost=3.0),
 }
-WORKLOAD_ORDER = ["tiny", "skew64", "split128", "tie64", "large256"]
+WORKLOAD_ORDER = ["tiny", "skew64", "split128", "tie64", "large256", "rank256"]
 
 TIE_GRID_STEPS = 16   # values k/4 for k = -16..16: 33 distinct BF16 values in [-4, 4]
 
