@@ -149,6 +149,48 @@ __device__ __forceinline__ int med3_i32(int a, int b, int c) {
   return r;
 }
 
+// ------------------------------------------------------- float keys --
+// Routing keys are binary32 bit patterns kept in int registers and ordered
+// as floats.  A key is finite or the sentinel -inf, never NaN, and the keys
+// of one row never include both +0 and -0, so the float order is a strict
+// total order on them whatever their signs.  Maximum and median are written
+// as the instructions themselves: the compiler's IEEE-mode maximum would
+// first quieten both operands with an extra instruction each.
+constexpr int kKeyNone = (int)0xFF800000u;   // -inf: below every key
+
+__device__ __forceinline__ int key_max(int a, int b) {
+  int r;
+  asm volatile("v_max_f32 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
+  return r;
+}
+__device__ __forceinline__ int key_med3(int a, int b, int c) {
+  int r;
+  asm volatile("v_med3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
+  return r;
+}
+__device__ __forceinline__ bool key_lt(int a, int b) { return __int_as_float(a) < __int_as_float(b); }
+
+// Float maximum of the keys over aligned groups of G lanes, one DPP maximum
+// per level as in group_max_i32.  Each level starts with two wait states, so
+// the DPP read never follows a VALU write of its source register too closely.
+template <int G>
+__device__ __forceinline__ int group_max_key(int x) {
+  if constexpr (G >= 2)
+    asm volatile("s_nop 1\n\tv_max_f32_dpp %0, %0, %0 quad_perm:[1,0,3,2] row_mask:0xf bank_mask:0xf bound_ctrl:1"
+                 : "+v"(x));
+  if constexpr (G >= 4)
+    asm volatile("s_nop 1\n\tv_max_f32_dpp %0, %0, %0 quad_perm:[2,3,0,1] row_mask:0xf bank_mask:0xf bound_ctrl:1"
+                 : "+v"(x));
+  if constexpr (G >= 8)
+    asm volatile("s_nop 1\n\tv_max_f32_dpp %0, %0, %0 row_half_mirror row_mask:0xf bank_mask:0xf bound_ctrl:1"
+                 : "+v"(x));
+  if constexpr (G >= 16)
+    asm volatile("s_nop 1\n\tv_max_f32_dpp %0, %0, %0 row_mirror row_mask:0xf bank_mask:0xf bound_ctrl:1"
+                 : "+v"(x));
+  static_assert(G <= 16, "group reductions cover at most 16 lanes");
+  return x;
+}
+
 // ------------------------------------------------------- partition walk --
 // Calls f(p, s0, s1) for every piece of [r0, r1) lying in one partition and
 // holding at most kSegMax rows.  Uniform across the block.

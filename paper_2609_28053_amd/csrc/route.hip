@@ -5,15 +5,18 @@
 // Fast kernel (K <= kFastKmax).  A row of E logits is spread over G lanes,
 // each holding N = E/G experts as N/4 8-byte pieces.  Per element it forms a
 // 32-bit key: the binary32 bits of s = z + b with the low byte replaced by
-// 255 - e, and keeps a sorted list of its kList largest keys (one v_max and
-// kList-1 v_med3 per element).
+// 255 - e, and keeps a sorted list of its kList largest keys (one maximum and
+// kList-1 medians per element).  Keys are compared as floats, so negative
+// scores order correctly; the key's sum takes -0 in b as +0, so a score of
+// -0 keys as +0 and the two zeros share one run of keys.
 // K+2 extraction rounds then take the group maximum of the list heads with
-// DPP and pop the winner, refilling a lane whose list runs dry.  For a
-// positive tau, signed key order is score order except between scores that
-// agree in their top 24 bits; extraction continues until the last key leaves
-// the top-24-bit run of rank K, the winners' exact scores are recomputed from
-// z and b, and a row whose extracted scores are not in exact order is sorted
-// exactly.  Rows with tau <= 0 take the exact 64-bit path.
+// DPP and pop the winner, refilling a lane whose list runs dry.  Key order is
+// score order except between scores that agree in their top 24 bits;
+// extraction continues until the last key leaves the top-24-bit run of rank
+// K, the winners' exact scores are recomputed from z and b, and a row whose
+// extracted scores are not in exact order is sorted exactly.  A block whose
+// bias has |b| >= 2^119 (where z + b could overflow) takes the exact 64-bit
+// path for every row.
 //
 // Generic kernel (any K < E): K+1 rounds over exact 64-bit keys.
 #include "eqb_internal.hpp"
@@ -31,15 +34,17 @@ template <int E> struct FastCfg { static constexpr int G = E >= 64 ? 8 : E / 8; 
 // adjacent BF16 values give scores more than 256 binary32 ulps of s apart,
 // so at most one BF16 value maps to H; it is bf16(s_mid - b) with s_mid the
 // middle of the 256-ulp interval, and it is accepted only after
-// fl32(z + b) is checked to reproduce H.  *ok reports the check; otherwise z
-// must be read from memory (z_or_load).
+// fl32(z + b) is checked to reproduce H.  The two zeros are the exception:
+// +0 and -0 give the same sum, and which one z is decides the sign of a zero
+// tau, so a zero is never accepted.  *ok reports the check; otherwise z must
+// be read from memory (z_or_load).
 __device__ __forceinline__ uint32_t z_from_key(int key, float b, bool* ok) {
   const uint32_t kb = (uint32_t)key;
   const float s_mid = __uint_as_float((kb & 0xFFFFFF00u) | 0x80u);
   const uint32_t zc = bf16x2_bits(s_mid - b, 0.0f) & 0xFFFFu;
   const uint32_t sc = __float_as_uint(__uint_as_float(zc << 16) + b);
   const int ez = (int)((zc >> 7) & 0xFFu), es = (int)((kb >> 23) & 0xFFu);
-  *ok = ((sc ^ kb) < 256u) && (ez >= es - 6) && ((zc & 0x7F80u) != 0x7F80u);
+  *ok = ((sc ^ kb) < 256u) && (ez >= es - 6) && ((zc & 0x7F80u) != 0x7F80u) && ((zc & 0x7FFFu) != 0u);
   return zc;
 }
 
@@ -65,12 +70,12 @@ __device__ __forceinline__ V& at(B* base, uint32_t byte_off) {
   return *reinterpret_cast<V*>(reinterpret_cast<char*>(const_cast<std::remove_const_t<B>*>(base)) + byte_off);
 }
 
-// Insert x into the sorted list L[0] >= ... >= L[n-1] (one max, n-1 med3).
+// Insert key x into the sorted list L[0] >= ... >= L[n-1] (one max, n-1 med3).
 template <int n>
 __device__ __forceinline__ void list_insert(int (&L)[n], int x) {
 #pragma unroll
-  for (int j = n - 1; j > 0; --j) L[j] = med3_i32(L[j - 1], L[j], x);
-  L[0] = max(L[0], x);
+  for (int j = n - 1; j > 0; --j) L[j] = key_med3(L[j - 1], L[j], x);
+  L[0] = key_max(L[0], x);
 }
 
 template <int E, int KT>
@@ -91,7 +96,8 @@ __global__ __launch_bounds__(kBlock) void route_fast_kernel(
 
   __shared__ uint32_t sh_hist[hist_words<E>()];
   __shared__ uint32_t sh_load[E];
-  __shared__ float sh_b[E];
+  __shared__ float sh_b[E];             // b as given: exact scores and tau
+  __shared__ float sh_bk[E];            // b with -0 as +0: the keys' sums
   __shared__ uint2 sh_rank[kWaves][R][kRmax];   // (score bits, zbits << 16 | e) in rank order
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -99,19 +105,26 @@ __global__ __launch_bounds__(kBlock) void route_fast_kernel(
 
   // Piece q of this lane covers experts ex(q) .. ex(q)+3, so the G lanes of a
   // row read 8*G contiguous bytes per piece.  b is read from LDS, four experts
-  // at a time.
+  // at a time (bias4: the keys' copy, bias4x: b as given).
   auto ex = [&](int q) -> int { return q * 4 * G + g * 4; };
   // bytes 255 - e for the four experts of a piece (ex is a multiple of 4, no borrow)
   auto idxpk = [&](int q) -> uint32_t { return 0xFCFDFEFFu - (uint32_t)ex(q) * 0x01010101u; };
-  auto bias4 = [&](int q) -> float4 { return *reinterpret_cast<const float4*>(&sh_b[ex(q)]); };
+  auto bias4 = [&](int q) -> float4 { return *reinterpret_cast<const float4*>(&sh_bk[ex(q)]); };
+  auto bias4x = [&](int q) -> float4 { return *reinterpret_cast<const float4*>(&sh_b[ex(q)]); };
   auto pick = [](const float4& v, int i) -> float { return i == 0 ? v.x : i == 1 ? v.y : i == 2 ? v.z : v.w; };
 
   for (int w = threadIdx.x; w < hist_words<E>(); w += kBlock) sh_hist[w] = 0;
+  int fits = 1;
   for (int e = threadIdx.x; e < E; e += kBlock) {
     sh_load[e] = 0;
-    sh_b[e] = b[e];
+    const float bv = b[e];
+    sh_b[e] = bv;
+    sh_bk[e] = (__float_as_uint(bv) == 0x80000000u) ? 0.0f : bv;
+    fits &= (int)(fabsf(bv) < 0x1p119f);
   }
-  __syncthreads();
+  // |z| <= 2^128 - 2^120 for a finite BF16 z, so with |b| < 2^119 every sum
+  // z + b is finite and every key is a finite float.
+  const bool bias_ok = __syncthreads_and(fits) != 0;
 
   int64_t r0, r1;
   block_rows(T, rows_per_block, &r0, &r1);
@@ -126,7 +139,7 @@ __global__ __launch_bounds__(kBlock) void route_fast_kernel(
   // Rebuild a lane's sorted list from its keys strictly below thr.
   auto rebuild = [&](const float (&zf)[N], int thr, int (&L)[kList]) __attribute__((always_inline)) {
 #pragma unroll
-    for (int j = 0; j < kList; ++j) L[j] = INT_MIN;
+    for (int j = 0; j < kList; ++j) L[j] = kKeyNone;
 #pragma unroll
     for (int q = 0; q < NQ; ++q) {
       const float4 bq = bias4(q);
@@ -134,7 +147,7 @@ __global__ __launch_bounds__(kBlock) void route_fast_kernel(
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int x = key_of(zf[q * 4 + i], pick(bq, i), ipk, i);
-        list_insert(L, (x < thr) ? x : INT_MIN);
+        list_insert(L, key_lt(x, thr) ? x : kKeyNone);
       }
     }
   };
@@ -160,7 +173,7 @@ __global__ __launch_bounds__(kBlock) void route_fast_kernel(
     }
     int L[kList];
 #pragma unroll
-    for (int j = 0; j < kList; ++j) L[j] = INT_MIN;
+    for (int j = 0; j < kList; ++j) L[j] = kKeyNone;
 #pragma unroll
     for (int q = 0; q < NQ; ++q) {
       const float4 bq = bias4(q);
@@ -174,10 +187,10 @@ __global__ __launch_bounds__(kBlock) void route_fast_kernel(
       const bool win = (L[0] == M);
 #pragma unroll
       for (int j = 0; j < kList - 1; ++j) L[j] = win ? L[j + 1] : L[j];
-      L[kList - 1] = win ? INT_MIN : L[kList - 1];
+      L[kList - 1] = win ? kKeyNone : L[kList - 1];
     };
     // Rows whose ranks are staged in LDS: run past rank K+1, equal top-24-bit
-    // keys, a list that ran dry, or (slow) a cutoff that is not positive.
+    // keys or a list that ran dry; (slow) rows the keys cannot settle.
     bool staged = false, slow = false;
     int nrank = 0;
     float tv = 0.0f;          // tau of this lane's row (common rows)
@@ -185,16 +198,16 @@ __global__ __launch_bounds__(kBlock) void route_fast_kernel(
     uint32_t zown[RSLOT];
 #pragma unroll
     for (int s = 0; s < RSLOT; ++s) {
-      rk[s] = INT_MIN;
+      rk[s] = kKeyNone;
       zown[s] = 0;
     }
 
     if constexpr (KT > 0) {
-      int mK = INT_MIN, mK1 = INT_MIN, prev = INT_MIN;
+      int mK = kKeyNone, mK1 = kKeyNone, prev = kKeyNone;
       bool near = false;      // two adjacent extracted keys share their top 24 bits
 #pragma unroll
       for (int k = 0; k < KT + 2; ++k) {
-        const int M = group_max_i32<G>(L[0]);
+        const int M = group_max_key<G>(L[0]);
         if (k < KT + 1) pop(M);
         rk[k / G] = (g == k % G) ? M : rk[k / G];
         if (k > 0) near |= ((uint32_t)(M ^ prev) < 256u);
@@ -210,14 +223,16 @@ __global__ __launch_bounds__(kBlock) void route_fast_kernel(
         uint32_t zc = 0;
         int e = 0;
         if (valid && k <= KT) {
-          e = 255 - (rk[s] & 0xFF);
-          zc = z_from_key(rk[s], sh_b[e], &ok);
+          // below E for every key of the row; the clamp keeps a row whose
+          // keys cannot be trusted (it goes slow) inside its own logits
+          e = min(255 - (rk[s] & 0xFF), E - 1);
+          zc = z_from_key(rk[s], sh_bk[e], &ok);
         }
         zown[s] = z_or_load(zc, ok, &at<uint16_t>(seg_z, (t * E + e) * 2u));
       }
       const int tauhi = mK >> 8;
-      const bool dry = group_max_i32<G>((int)(L[0] == INT_MIN)) != 0;
-      slow = valid && tauhi <= 0;
+      const bool dry = group_max_i32<G>((int)(L[0] == kKeyNone)) != 0;
+      slow = valid && !bias_ok;
       staged = valid && !slow && (near || dry);
       nrank = KT + 2;
       if (__any(staged)) {
@@ -236,12 +251,12 @@ __global__ __launch_bounds__(kBlock) void route_fast_kernel(
           for (int k = KT + 2; k < kRmax; ++k) {
             if (!__any(ext)) break;
             // a lane whose list ran dry may hold the next key
-            const bool dry_now = group_max_i32<G>((int)(L[0] == INT_MIN)) != 0;
+            const bool dry_now = group_max_i32<G>((int)(L[0] == kKeyNone)) != 0;
             if (ext && dry_now) {
               bad = true;
               ext = false;
             }
-            const int M = group_max_i32<G>(L[0]);
+            const int M = group_max_key<G>(L[0]);
             if (ext) {
               if (g == 0) myrank[k].x = (uint32_t)M;
               nrank = k + 1;
@@ -260,11 +275,10 @@ __global__ __launch_bounds__(kBlock) void route_fast_kernel(
           if (staged && k < nrank) {
             const int key = (int)myrank[k].x;
             const int e = 255 - (key & 0xFF);
-            const float bv = sh_b[e];
             bool ok;
-            uint32_t zb = z_from_key(key, bv, &ok);
+            uint32_t zb = z_from_key(key, sh_bk[e], &ok);
             if (!ok) zb = seg_z[t * E + e];
-            const uint32_t sb = __float_as_uint(__uint_as_float(zb << 16) + bv);
+            const uint32_t sb = __float_as_uint(__uint_as_float(zb << 16) + sh_b[e]);
             myrank[k] = make_uint2(sb, (zb << 16) | (uint32_t)e);
           }
         }
@@ -276,14 +290,14 @@ __global__ __launch_bounds__(kBlock) void route_fast_kernel(
 #pragma unroll 1
       for (int k = 0; k < kRmax; ++k) {
         if (!__any(!done)) break;
-        const int M = group_max_i32<G>(L[0]);
+        const int M = group_max_key<G>(L[0]);
         pop(M);
-        const bool dry = (L[0] == INT_MIN) && (M != INT_MIN);
+        const bool dry = (L[0] == kKeyNone) && (M != kKeyNone);
         if (__any(dry && !done)) {
           if (dry && !done) rebuild(zf, M, L);
         }
         if (!done) {
-          if (M == INT_MIN) {
+          if (M == kKeyNone) {
             done = true;
           } else {
             if (g == 0) myrank[k].x = (uint32_t)M;
@@ -293,7 +307,7 @@ __global__ __launch_bounds__(kBlock) void route_fast_kernel(
           }
         }
       }
-      slow = valid && (!done || tauhi <= 0);
+      slow = valid && (!done || !bias_ok);
       staged = valid && !slow;
       lds_wave_sync();
 #pragma unroll
@@ -309,16 +323,19 @@ __global__ __launch_bounds__(kBlock) void route_fast_kernel(
       lds_wave_sync();
     }
 
-    // ---- staged rows: sort the extracted ranks exactly where top-24-bit keys tie
+    // ---- staged rows: sort the extracted ranks exactly where key order and
+    // exact order differ (only inside a run of equal top-24-bit keys)
+    // rank order of two staged entries: higher score, then lower expert
+    auto before = [](uint2 a, uint2 c) -> bool {
+      const float fa = __uint_as_float(a.x), fc = __uint_as_float(c.x);
+      return fa > fc || (fa == fc && (a.y & 0xFF) < (c.y & 0xFF));
+    };
     if (__any(staged)) {
       bool coll = false;
 #pragma unroll
       for (int s = 0; s < RSLOT; ++s) {
         const int k = s * G + g;
-        if (staged && k + 1 < nrank) {
-          const uint2 a = myrank[k], c = myrank[k + 1];
-          coll |= ((a.x >> 8) == (c.x >> 8)) && (a.x != c.x);
-        }
+        if (staged && k + 1 < nrank) coll |= !before(myrank[k], myrank[k + 1]);
       }
       const bool coll_row = group_max_i32<G>((int)coll) != 0;
       if (coll_row && g == 0) {
@@ -327,8 +344,7 @@ __global__ __launch_bounds__(kBlock) void route_fast_kernel(
           int j = i - 1;
           while (j >= 0) {
             const uint2 u = myrank[j];
-            const bool worse = ((int)u.x < (int)v.x) || (u.x == v.x && (u.y & 0xFF) > (v.y & 0xFF));
-            if (!worse) break;
+            if (!before(v, u)) break;
             myrank[j + 1] = u;
             --j;
           }
@@ -346,7 +362,7 @@ __global__ __launch_bounds__(kBlock) void route_fast_kernel(
           uint64_t m = 0;
 #pragma unroll
           for (int q = 0; q < NQ; ++q) {
-            const float4 bq = bias4(q);
+            const float4 bq = bias4x(q);
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
               // rebuilt every round instead of being held in 2*N registers

@@ -86,7 +86,8 @@ def oracle_for(name, T=None, P=None):
 
 # ------------------------------------------------- multi-tile, ragged -----
 SMALL = [("tiny", 4096 + 517, 3), ("skew64", 20011, 4), ("split128", 9973, 8),
-         ("tie64", 16411, 2), ("large256", 7001, 16)]
+         ("tie64", 16411, 2), ("large256", 7001, 16), ("neg256", 12007, 4),
+         ("signs64", 9001, 2)]
 
 
 @pytest.mark.parametrize("name,T,P", SMALL, ids=[s[0] for s in SMALL])
@@ -127,16 +128,53 @@ def test_every_E_and_K_extremes(eqb, E):
             assert_parity(gpu_layer(eqb, z, b, K, off), O.run_layer(z, b, K, off), K)
 
 
-def test_all_ties_constant_logits(eqb):
+@pytest.mark.parametrize("zbits", [0x3F00, 0xBF00, 0x8000], ids=["half", "minus_half", "minus_zero"])
+@pytest.mark.parametrize("bzero", [0.0, -0.0], ids=["b_plus0", "b_minus0"])
+def test_all_ties_constant_logits(eqb, zbits, bzero):
     for E, K in ((8, 2), (64, 6), (256, 8)):
         T = 3000
-        z = np.full((T, E), 0x3F00, np.uint16)                 # every logit 0.5
-        b = np.zeros(E, np.float32)
-        say(f"constant logits E={E}")
+        z = np.full((T, E), zbits, np.uint16)                   # every logit equal
+        b = np.full(E, bzero, np.float32)
+        say(f"constant logits {zbits:#06x} b={bzero} E={E}")
         want = O.run_layer(z, b, K)
         got = gpu_layer(eqb, z, b, K, None)
         assert_parity(got, want, K)
         assert np.all(got["idx"] == np.arange(K))               # lower index wins every tie
+
+
+def test_zero_scores_of_both_signs(eqb):
+    # s = -0 where z = -0 meets b = -0, +0 elsewhere: every score is a zero,
+    # the zeros tie, and the lower index wins
+    rng = np.random.default_rng(11)
+    for E, K in ((64, 4), (256, 8)):
+        T = 4099
+        z = np.where(rng.integers(0, 2, (T, E)).astype(bool), 0x8000, 0x0000).astype(np.uint16)
+        b = np.where(rng.integers(0, 2, E).astype(bool), np.float32(-0.0), np.float32(0.0))
+        say(f"signed-zero scores E={E}")
+        want = O.run_layer(z, b, K)
+        got = gpu_layer(eqb, z, b, K, None)
+        assert_parity(got, want, K)
+        assert np.all(got["idx"] == np.arange(K))
+
+
+@pytest.mark.parametrize("E,K", [(64, 2), (128, 6), (256, 8), (32, 3)])
+def test_huge_bias_takes_the_exact_path(eqb, E, K):
+    # |b| >= 2^119 sends every row of the block through exact 64-bit keys;
+    # with z at the BF16 maximum, z + b overflows to +inf for one expert
+    rng = np.random.default_rng(E + K)
+    T = 5003
+    z = O.f32_to_bf16_rne((rng.standard_normal((T, E)) - 2.0).astype(np.float32))
+    b = (rng.standard_normal(E) * 0.3).astype(np.float32)
+    b[3] = np.float32(2.0 ** 120)
+    say(f"bias 2^120 E={E} K={K}")
+    assert_parity(gpu_layer(eqb, z, b, K, None), O.run_layer(z, b, K), K)
+    b[5] = np.float32(3.0e38)
+    z[::7, 5] = 0x7F7F                                            # z + b = +inf on these rows
+    say(f"bias overflow E={E} K={K}")
+    want = O.run_layer(z, b, K)
+    assert np.isinf(want["tau"]).sum() == 0 and np.isposinf(
+        O.bf16_to_f32(z[::7, 5]).astype(np.float32) + b[5]).all()
+    assert_parity(gpu_layer(eqb, z, b, K, None), want, K)
 
 
 def test_signed_zeros_and_subnormals(eqb):

@@ -8,7 +8,10 @@ The paper trains a 7.5B MoE with E=256 routed experts and K=6 (Appendix E,
 "Model, training, and evaluation"); its router logits come from trained
 weights on a pretraining corpus that is not available.  The recipes below
 stand in for those logits with normal draws plus a per-expert offset (expert
-skew), a few boosted tokens, and a tie-heavy grid.
+skew), a few boosted tokens, and a tie-heavy grid.  A sigmoid router's logits
+sit mostly below zero (its selected experts score well under 1/2), so one
+workload is shifted down until the cutoffs straddle zero, and one puts a grid
+of non-positive logits under a bias of signed zeros.
 
 Every array is produced deterministically from (config, seed):
   * a main generator ``default_rng(seed)`` draws, in this order, the
@@ -43,8 +46,9 @@ class Workload:
     K: int
     P: int
     seed: int
-    kind: str            # "normal", "tie", "boost"
+    kind: str            # "normal", "tie", "boost", "negtie"
     z_sigma: float = 1.0
+    z_mean: float = 0.0
     off_sigma: float = 0.0
     b_sigma: float = 0.0
     b_bf16: bool = False
@@ -61,8 +65,10 @@ class Workload:
         return -(-self.T * self.K // self.E)
 
 
-# The five workloads: tiny (E=8), skewed E=64, random split E=128,
-# tie-heavy grid E=64, and the large E=256 layer with boosted tokens.
+# tiny (E=8), skewed E=64, random split E=128, tie-heavy grid E=64, the large
+# E=256 layer with boosted tokens and one rank's share of it, logits centred
+# below zero (cutoffs of both signs), and non-positive ties under a bias of
+# +0 and -0.
 WORKLOADS = {
     "tiny": Workload("tiny", T=4096, E=8, K=2, P=1, seed=0, kind="normal",
                      z_sigma=1.0, off_sigma=0.5, b_sigma=0.1),
@@ -80,8 +86,16 @@ WORKLOADS = {
     "rank256": Workload("rank256", T=147456, E=256, K=6, P=1, seed=5, kind="boost",
                         z_sigma=1.0, off_sigma=0.7, b_sigma=0.1,
                         boost_frac=0.05, boost=3.0),
+    # logits of a sigmoid router, shifted down by 2.375: about two thirds of
+    # the cutoffs are negative, and most rows mix scores of both signs
+    "neg256": Workload("neg256", T=1048576, E=256, K=8, P=4, seed=6, kind="boost",
+                       z_sigma=1.0, z_mean=-2.375, off_sigma=0.7, b_sigma=0.1,
+                       boost_frac=0.05, boost=3.0),
+    # z uniform over k/4, k = -16..0, zero's sign a fair coin; b is +0 or -0
+    # per expert: exact ties on non-positive scores, zero cutoffs of both signs
+    "signs64": Workload("signs64", T=262144, E=64, K=4, P=2, seed=7, kind="negtie"),
 }
-WORKLOAD_ORDER = ["tiny", "skew64", "split128", "tie64", "large256", "rank256"]
+WORKLOAD_ORDER = ["tiny", "skew64", "split128", "tie64", "large256", "rank256", "neg256", "signs64"]
 
 TIE_GRID_STEPS = 16   # values k/4 for k = -16..16: 33 distinct BF16 values in [-4, 4]
 
@@ -105,8 +119,9 @@ def partition_offsets(w: Workload, rng: np.random.Generator) -> np.ndarray:
 
 def _z_chunk(w: Workload, c: int, rows: int, off: np.ndarray, batch: int = 0) -> np.ndarray:
     g = np.random.default_rng([w.seed, c] if batch == 0 else [w.seed, batch, c])
-    if w.kind == "tie":
-        k = g.integers(-TIE_GRID_STEPS, TIE_GRID_STEPS + 1, size=(rows, w.E))
+    if w.kind in ("tie", "negtie"):
+        top = TIE_GRID_STEPS if w.kind == "tie" else 0
+        k = g.integers(-TIE_GRID_STEPS, top + 1, size=(rows, w.E))
         neg = g.integers(0, 2, size=(rows, w.E)).astype(bool)
         bits = _to_bf16_bits(k.astype(np.float32) / 4.0)
         bits[(k == 0) & neg] = 0x8000     # zero's sign is a fair coin: -0 and +0 both occur
@@ -114,6 +129,8 @@ def _z_chunk(w: Workload, c: int, rows: int, off: np.ndarray, batch: int = 0) ->
     x = g.standard_normal((rows, w.E), dtype=np.float32)
     if w.z_sigma != 1.0:
         x *= np.float32(w.z_sigma)
+    if w.z_mean != 0.0:
+        x += np.float32(w.z_mean)
     if w.off_sigma != 0.0:
         x += off[None, :]
     if w.kind == "boost":
@@ -138,6 +155,8 @@ def generate(w: Workload, threads: Optional[int] = None, batch: int = 0):
         b = rng.standard_normal(w.E, dtype=np.float32) * np.float32(w.b_sigma)
         if w.b_bf16:
             b = (_to_bf16_bits(b).astype(np.uint32) << 16).view(np.float32)
+    elif w.kind == "negtie":
+        b = np.where(rng.integers(0, 2, size=w.E).astype(bool), np.float32(-0.0), np.float32(0.0))
     else:
         b = np.zeros(w.E, np.float32)
     part_off = partition_offsets(w, rng)
