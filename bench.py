@@ -161,6 +161,28 @@ def lei_leg(w, eqb, torch, lay, zt, part_off, stream, reps=10):
             "router_backward_frac_of_peak": bwd_gbs / HBM_PEAK_GBS, "eta": 2e-5, "c": 1.0}
 
 
+def signs_leg(torch, zt, lay, run_step, reps=10, shift=4.0):
+    """The whole step on the step's logits shifted down by `shift`, which
+    makes every cutoff negative: a sigmoid router's logits sit mostly below
+    zero, and the path should not depend on the sign of tau.  The shifted copy
+    is made on the device by torch (input preparation, finished before the
+    timed steps); stage times come from events as in the main measurement."""
+    zs = (zt.view(torch.bfloat16).float() - shift).to(torch.bfloat16).view(torch.int16)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        run_step(None, zs)
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(6)] for _ in range(reps)]
+    for i in range(reps):
+        run_step(evs[i], zs)
+    torch.cuda.synchronize()
+    frac = float((lay.tau <= 0).float().mean().item())
+    del zs
+    return {"shift": -shift, "tau_nonpositive_frac": frac,
+            "route_hist1_ms": float(np.mean([e[1].elapsed_time(e[2]) for e in evs])),
+            "margin_hist2_ms": float(np.mean([e[3].elapsed_time(e[4]) for e in evs])),
+            "step_ms_median": float(np.median([e[0].elapsed_time(e[5]) for e in evs]))}
+
+
 def variants_leg(w, eqb, torch, zt, bt, lay, part_off):
     """The statistics EQB is compared with (Sec. 2), on the same batch: the
     rank-averaged quantile (P shards, and P/4 shards to show that it depends
@@ -242,18 +264,19 @@ def main():
     stream = torch.cuda.Stream(device=dev)     # default priority
     lay = eqb.Layer(w.T, w.E, w.K, w.P, device=dev)
 
-    def step(ev=None):
+    def step(ev=None, zin=None):
+        zin = zt if zin is None else zin
         rec = (lambda i: ev[i].record(stream)) if ev else (lambda i: None)
         rec(0)
         lay._counts.zero_()
         rec(1)
-        eqb.eqb_route_topk(zt, bt, w.K, lay.topk_idx, lay.topk_score, lay.tau, part_off,
+        eqb.eqb_route_topk(zin, bt, w.K, lay.topk_idx, lay.topk_score, lay.tau, part_off,
                            lay.load, lay.hist_hi, stream)
         rec(2)
         eqb.eqb_select_quantile(1, lay.hist_hi, r, lay.sel_hi, lay.rank_in_bin,
                                 hist_sum=lay.H, dev_status=lay.dev_status, stream=stream)
         rec(3)
-        eqb.eqb_margin_hist_pass2(zt, lay.tau, lay.sel_hi, lay.hist_lo, part_off, stream)
+        eqb.eqb_margin_hist_pass2(zin, lay.tau, lay.sel_hi, lay.hist_lo, part_off, stream)
         rec(4)
         eqb.eqb_select_quantile(2, lay.hist_lo, r, lay.sel_hi, lay.rank_in_bin, lay.sel_lo,
                                 lay.q_bf16, lay.b_next, hist_sum=lay.L, dev_status=lay.dev_status,
@@ -313,6 +336,8 @@ def main():
     if not args.no_legs:
         out["lei"] = lei_leg(w, eqb, torch, lay, zt, part_off, stream)
         out["variants"] = variants_leg(w, eqb, torch, zt, bt, lay, part_off)
+        with torch.cuda.stream(stream):
+            out["cutoff_signs"] = signs_leg(torch, zt, lay, step)
     if args.qb_steps > 0:
         del zt
         out["qb_loop"] = qb_loop_leg(w, eqb, torch, args.qb_steps, dev, part_off)
