@@ -116,9 +116,14 @@ __global__ __launch_bounds__(kBlock) void lei_inject_kernel(
 // ------------------------------------- router backward with LEI ---------
 // grad_z[t,e] = (g[t,e] + inj[p(t),e]) * sigmoid'(z[t,e]), where g[t,e] is
 // grad_score[t,k] for e = topk_idx[t,k] and 0 for the other experts.  G = E/8
-// lanes hold a row, 8 experts each (one 16-byte load of z, two of grad_z).
-// The K mixture gradients of a row are scattered into a per-wave LDS row
-// (zeroed first) and read back 8 at a time.
+// lanes hold a row, 8 experts each (one 16-byte load of z, two of grad_z),
+// and every lane works on kBwdU rows per step.  The K mixture gradients of a
+// row are scattered into a per-wave LDS row (zeroed first) and read back 8 at
+// a time.  With K <= G lane g of a row owns pair k = g, and the next step's
+// logits and pairs are loaded while a step is processed; a larger K reads its
+// pairs inside the step.
+constexpr int kBwdU = 2;
+
 template <int E>
 __global__ __launch_bounds__(kBlock) void lei_router_backward_kernel(
     const uint16_t* __restrict__ z, const int32_t* __restrict__ topk_idx, const float* __restrict__ grad_score,
@@ -126,49 +131,95 @@ __global__ __launch_bounds__(kBlock) void lei_router_backward_kernel(
     int64_t rows_per_block) {
   constexpr int G = E / 8;
   constexpr int R = 64 / G;
-  constexpr int ROWS = kWaves * R;
-  __shared__ __align__(16) float sh_g[kWaves][R][E];
+  constexpr int ROWS = kWaves * R * kBwdU;
+  __shared__ __align__(16) float sh_g[kWaves][kBwdU][R][E];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int g = lane % G, rr = lane / G;
   const int e0 = g * 8;
-  float* myrow = sh_g[wave][rr];
+  const bool one_pair = K <= G;
   int64_t r0, r1;
   block_rows(T, rows_per_block, &r0, &r1);
   for_each_segment(r0, r1, pt, [&](int p, int64_t s0, int64_t s1) {
     float d[8];
 #pragma unroll
     for (int j = 0; j < 8; ++j) d[j] = inj ? inj[(int64_t)p * E + e0 + j] : 0.0f;
+    auto row_of = [&](int64_t base, int u) -> int64_t { return base + (int64_t)(u * kWaves + wave) * R + rr; };
+    // logits and this lane's pair of its rows at step base
+    auto load = [&](int64_t base, uint4 (&zw)[kBwdU], int (&e)[kBwdU], float (&gv)[kBwdU]) {
+#pragma unroll
+      for (int u = 0; u < kBwdU; ++u) {
+        const int64_t t = row_of(base, u);
+        zw[u] = make_uint4(0, 0, 0, 0);
+        e[u] = -1;
+        gv[u] = 0.0f;
+        if (t < s1) {
+          zw[u] = *reinterpret_cast<const uint4*>(z + t * E + e0);
+          if (one_pair && g < K) {
+            e[u] = topk_idx[t * K + g];
+            gv[u] = grad_score[t * K + g];
+          }
+        }
+      }
+    };
+    uint4 zn[kBwdU];
+    int en[kBwdU];
+    float gn[kBwdU];
+    load(s0, zn, en, gn);
     for (int64_t base = s0; base < s1; base += ROWS) {
-      const int64_t t = base + wave * R + rr;
-      const bool valid = t < s1;
-      uint4 zw = make_uint4(0, 0, 0, 0);
-      if (valid) zw = *reinterpret_cast<const uint4*>(z + t * E + e0);
-      // scatter the row's mixture gradients
-      *reinterpret_cast<float4*>(myrow + e0) = make_float4(0.f, 0.f, 0.f, 0.f);
-      *reinterpret_cast<float4*>(myrow + e0 + 4) = make_float4(0.f, 0.f, 0.f, 0.f);
+      uint4 zw[kBwdU];
+      int ec[kBwdU];
+      float gc[kBwdU];
+#pragma unroll
+      for (int u = 0; u < kBwdU; ++u) {
+        zw[u] = zn[u];
+        ec[u] = en[u];
+        gc[u] = gn[u];
+      }
+      if (base + ROWS < s1) load(base + ROWS, zn, en, gn);
+      // scatter the rows' mixture gradients
+#pragma unroll
+      for (int u = 0; u < kBwdU; ++u) {
+        float* myrow = sh_g[wave][u][rr];
+        *reinterpret_cast<float4*>(myrow + e0) = make_float4(0.f, 0.f, 0.f, 0.f);
+        *reinterpret_cast<float4*>(myrow + e0 + 4) = make_float4(0.f, 0.f, 0.f, 0.f);
+      }
       lds_wave_sync();
-      if (valid) {
-        for (int k = g; k < K; k += G) {
-          const int e = topk_idx[t * K + k];
-          if (e >= 0 && e < E) myrow[e] = grad_score[t * K + k];
+#pragma unroll
+      for (int u = 0; u < kBwdU; ++u) {
+        const int64_t t = row_of(base, u);
+        float* myrow = sh_g[wave][u][rr];
+        if (t < s1) {
+          if (one_pair) {
+            if (ec[u] >= 0 && ec[u] < E) myrow[ec[u]] = gc[u];
+          } else {
+            for (int k = g; k < K; k += G) {
+              const int e = topk_idx[t * K + k];
+              if (e >= 0 && e < E) myrow[e] = grad_score[t * K + k];
+            }
+          }
         }
       }
       lds_wave_sync();
-      const float4 ga = *reinterpret_cast<const float4*>(myrow + e0);
-      const float4 gb = *reinterpret_cast<const float4*>(myrow + e0 + 4);
-      const float gm[8] = {ga.x, ga.y, ga.z, ga.w, gb.x, gb.y, gb.z, gb.w};
-      const uint32_t w4[4] = {zw.x, zw.y, zw.z, zw.w};
-      float o[8];
 #pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const float zf = (j & 1) ? bf16_hi(w4[j >> 1]) : bf16_lo(w4[j >> 1]);
-        o[j] = (gm[j] + d[j]) * sigmoid_prime_fast(zf);
+      for (int u = 0; u < kBwdU; ++u) {
+        const int64_t t = row_of(base, u);
+        const float* myrow = sh_g[wave][u][rr];
+        const float4 ga = *reinterpret_cast<const float4*>(myrow + e0);
+        const float4 gb = *reinterpret_cast<const float4*>(myrow + e0 + 4);
+        const float gm[8] = {ga.x, ga.y, ga.z, ga.w, gb.x, gb.y, gb.z, gb.w};
+        const uint32_t w4[4] = {zw[u].x, zw[u].y, zw[u].z, zw[u].w};
+        float o[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          const float zf = (j & 1) ? bf16_hi(w4[j >> 1]) : bf16_lo(w4[j >> 1]);
+          o[j] = (gm[j] + d[j]) * sigmoid_prime_fast(zf);
+        }
+        if (t < s1) {
+          *reinterpret_cast<float4*>(grad_z + t * E + e0) = make_float4(o[0], o[1], o[2], o[3]);
+          *reinterpret_cast<float4*>(grad_z + t * E + e0 + 4) = make_float4(o[4], o[5], o[6], o[7]);
+        }
       }
-      if (valid) {
-        *reinterpret_cast<float4*>(grad_z + t * E + e0) = make_float4(o[0], o[1], o[2], o[3]);
-        *reinterpret_cast<float4*>(grad_z + t * E + e0 + 4) = make_float4(o[4], o[5], o[6], o[7]);
-      }
-      lds_wave_sync();          // the row buffer is rewritten by the next step
+      lds_wave_sync();          // the row buffers are rewritten by the next step
     }
   });
 }
@@ -178,7 +229,7 @@ static void launch_backward_e(const uint16_t* z, const int32_t* idx, const float
                               int K, float* gz, const PartTable& pt, hipStream_t s) {
   int blocks;
   int64_t rpb;
-  grid_for(T, kWaves * (64 / (E / 8)), 2, &blocks, &rpb);
+  grid_for(T, kWaves * (64 / (E / 8)) * kBwdU, 2, &blocks, &rpb);
   lei_router_backward_kernel<E><<<blocks, kBlock, 0, s>>>(z, idx, gs, inj, T, K, gz, pt, rpb);
 }
 
