@@ -390,11 +390,20 @@ def qb_loop(batches, b0, K: int, part_off=None, stream=None):
     return steps
 
 
-def rank_averaged_qb(z, b, K: int, part_off=None, stream=None) -> dict:
+def _mark(marks, name):
+    """Record an event on the current stream after a stage, if asked."""
+    if marks is not None:
+        ev = torch.cuda.Event(enable_timing=True)
+        ev.record()
+        marks.append((name, ev))
+
+
+def rank_averaged_qb(z, b, K: int, part_off=None, stream=None, marks=None) -> dict:
     """Rank-averaged QB (Sec. 2): every shard's exact K/E quantile of its own
     margins, averaged over the shards and centred.  Returns host copies of
     the shards' quantiles (BF16 bits [P,E]), the average (binary64 [E]) and
-    the centred bias."""
+    the centred bias.  ``marks``, a list, receives (stage, event) pairs
+    recorded after each device stage."""
     T, E = z.shape
     P = 1 if part_off is None else len(part_off) - 1
     ctx = torch.cuda.stream(stream) if stream is not None else contextlib.nullcontext()
@@ -412,21 +421,28 @@ def rank_averaged_qb(z, b, K: int, part_off=None, stream=None) -> dict:
         q = torch.empty((P, E), dtype=torch.int16, device=dev)
         b_avg = torch.empty(E, dtype=torch.float64, device=dev)
         b_next = torch.empty(E, dtype=torch.float32, device=dev)
+        _mark(marks, "start")
         eqb_route_topk(z, b, K, idx, score, tau, part_off, None, hist[0])
+        _mark(marks, "route_hist1")
         eqb_select_quantile_local(1, hist[0], T, K, sel_hi, rib, part_off=part_off, dev_status=status)
+        _mark(marks, "select1_local")
         eqb_margin_hist_pass2_local(z, tau, sel_hi, hist[1], part_off)
+        _mark(marks, "hist2_local")
         eqb_select_quantile_local(2, hist[1], T, K, sel_hi, rib, sel_lo, q, part_off, status)
+        _mark(marks, "select2_local")
         eqb_rank_average(q, T, b_next, b_avg, part_off)
+        _mark(marks, "rank_average")
         return dict(bhat_p=q.cpu().numpy().view(np.uint16), b_avg=b_avg.cpu().numpy(),
                     b_next=b_next.cpu().numpy(), dev_status=int(status.item()))
 
 
-def histogram_qb(z, b, K: int, lo: float, hi: float, nbins: int, part_off=None, stream=None) -> dict:
+def histogram_qb(z, b, K: int, lo: float, hi: float, nbins: int, part_off=None, stream=None,
+                 marks=None) -> dict:
     """Fixed-resolution histogram QB (Sec. 2): margin counts over nbins
     uniform bins of [lo, hi), summed over the shards, the K/E quantile read
     off the sum by linear interpolation within its bin, then centred.
     Returns host copies of the counts [P,E,nbins], the estimate (binary64 [E])
-    and the centred bias."""
+    and the centred bias.  ``marks`` as for rank_averaged_qb."""
     T, E = z.shape
     P = 1 if part_off is None else len(part_off) - 1
     ctx = torch.cuda.stream(stream) if stream is not None else contextlib.nullcontext()
@@ -439,8 +455,12 @@ def histogram_qb(z, b, K: int, lo: float, hi: float, nbins: int, part_off=None, 
         status = torch.zeros(1, dtype=torch.int32, device=dev)
         est = torch.empty(E, dtype=torch.float64, device=dev)
         b_next = torch.empty(E, dtype=torch.float32, device=dev)
+        _mark(marks, "start")
         eqb_route_topk(z, b, K, idx, score, tau, part_off)
+        _mark(marks, "route")
         eqb_margin_hist_uniform(z, tau, lo, hi, hist, part_off)
+        _mark(marks, "uniform_hist")
         eqb_select_uniform(hist, eqb_rank(T, K, E), lo, hi, est, b_next, status)
+        _mark(marks, "select_uniform")
         return dict(counts=hist.cpu().numpy(), est=est.cpu().numpy(), b_next=b_next.cpu().numpy(),
                     dev_status=int(status.item()))
