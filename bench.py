@@ -17,6 +17,7 @@ import argparse
 import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -29,6 +30,12 @@ HBM_PEAK_GBS = 8000.0                     # MI355X HBM3E, vendor figure
 METRIC = "routing+EQB tokens/s per MoE layer; achieved HBM GB/s vs peak"
 CSRC = os.path.join(ROOT, "paper_2609_28053_amd", "csrc")
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "route_hist1_large256_traffic.txt")
+VALU_FILE = os.path.join(ROOT, "profiles", "route_fine_large256_valu_counters.txt")
+# Vector issue peak: 256 CUs x 4 SIMDs, a wave64 instruction occupies a
+# 16-lane SIMD for 4 cycles, 2.4 GHz: 256 * 4 * 16 * 2.4e9 lane-operations/s
+# (the vendor's 157.3 TFLOP/s FP32 figure counts an FMA as two and packed
+# FP32 as two more).
+VALU_PEAK_LANE_OPS = 256 * 4 * 16 * 2.4e9
 
 
 def route_bytes_per_token(E, K):
@@ -70,6 +77,27 @@ def read_traffic(T):
         return float(vals["hbm_bytes_per_launch"])
     except (KeyError, ValueError):
         return None
+
+
+def read_valu_per_element(T):
+    """Issued VALU instructions per (token, expert) of the route kernel, from
+    the committed SQ_INSTS_VALU summary, if it was taken on the current kernel
+    source and the same token count."""
+    if not os.path.exists(VALU_FILE):
+        return None
+    lines = open(VALU_FILE).read().splitlines()
+    head = " ".join(l for l in lines if l.startswith("#"))
+    m_hash = re.search(r"sources sha256\[:16\] = ([0-9a-f]{16})", head)
+    m_t = re.search(r"\bT=(\d+)", head)
+    if not m_hash or m_hash.group(1) != source_hash() or not m_t or int(m_t.group(1)) != T:
+        return None
+    section = None
+    for line in lines:
+        if line.startswith("## "):
+            section = line
+        elif section and "route_fast" in section and line.startswith("valu_per_element"):
+            return float(line.split("=", 1)[1])
+    return None
 
 
 def cpu_model():
@@ -315,6 +343,17 @@ def main():
     route_bytes = route_bytes_per_token(w.E, w.K) * w.T
     route_gbs = route_bytes / (stage_ms["route_hist1"] * 1e-3) / 1e9
     traffic = read_traffic(w.T)
+    # The route kernel is limited by vector instruction issue, not by HBM:
+    # its issued VALU (counted offline) over its live duration, against the
+    # issue peak.
+    vpe = read_valu_per_element(w.T)
+    valu_view = None
+    if vpe is not None:
+        ops = vpe * w.T * w.E
+        achieved = ops / (stage_ms["route_hist1"] * 1e-3)
+        valu_view = {"valu_per_element": vpe, "achieved_lane_ops_per_s": achieved,
+                     "peak_lane_ops_per_s": VALU_PEAK_LANE_OPS, "frac": achieved / VALU_PEAK_LANE_OPS,
+                     "source": os.path.relpath(VALU_FILE, ROOT)}
 
     out = {
         "metric": METRIC,
@@ -338,7 +377,8 @@ def main():
         "step_ms_events": step_ms,
         "roofline": {"kernel": "route_hist1", "bound": "hbm", "achieved": route_gbs,
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": route_gbs / HBM_PEAK_GBS,
-                     "traffic": traffic, "algorithmic_bytes": route_bytes},
+                     "traffic": traffic, "algorithmic_bytes": route_bytes,
+                     "valu_issue": valu_view},
     }
     if not args.no_legs:
         out["lei"] = lei_leg(w, eqb, torch, lay, zt, part_off, stream)
