@@ -155,17 +155,19 @@ __device__ __forceinline__ int med3_i32(int a, int b, int c) {
 // of one row never include both +0 and -0, so the float order is a strict
 // total order on them whatever their signs.  Maximum and median are written
 // as the instructions themselves: the compiler's IEEE-mode maximum would
-// first quieten both operands with an extra instruction each.
+// first quieten both operands with an extra instruction each.  They are
+// per-lane functions of their operands, so the asm is not volatile and the
+// compiler may schedule loads across it.
 constexpr int kKeyNone = (int)0xFF800000u;   // -inf: below every key
 
 __device__ __forceinline__ int key_max(int a, int b) {
   int r;
-  asm volatile("v_max_f32 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
+  asm("v_max_f32 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
   return r;
 }
 __device__ __forceinline__ int key_med3(int a, int b, int c) {
   int r;
-  asm volatile("v_med3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
+  asm("v_med3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
   return r;
 }
 __device__ __forceinline__ bool key_lt(int a, int b) { return __int_as_float(a) < __int_as_float(b); }
