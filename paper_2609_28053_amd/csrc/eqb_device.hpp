@@ -177,9 +177,13 @@ __device__ __forceinline__ bool key_lt(int a, int b) { return __int_as_float(a) 
 // the DPP read never follows a VALU write of its source register too closely.
 template <int G>
 __device__ __forceinline__ int group_max_key(int x) {
-  if constexpr (G >= 2)
-    asm volatile("s_nop 1\n\tv_max_f32_dpp %0, %0, %0 quad_perm:[1,0,3,2] row_mask:0xf bank_mask:0xf bound_ctrl:1"
-                 : "+v"(x));
+  if constexpr (G >= 2) {
+    // the first level writes a new register, so x itself needs no copy
+    int y;
+    asm volatile("s_nop 1\n\tv_max_f32_dpp %0, %1, %1 quad_perm:[1,0,3,2] row_mask:0xf bank_mask:0xf bound_ctrl:1"
+                 : "=v"(y) : "v"(x));
+    x = y;
+  }
   if constexpr (G >= 4)
     asm volatile("s_nop 1\n\tv_max_f32_dpp %0, %0, %0 quad_perm:[2,3,0,1] row_mask:0xf bank_mask:0xf bound_ctrl:1"
                  : "+v"(x));
@@ -191,6 +195,27 @@ __device__ __forceinline__ int group_max_key(int x) {
                  : "+v"(x));
   static_assert(G <= 16, "group reductions cover at most 16 lanes");
   return x;
+}
+
+// Value of lane S of every aligned group of G lanes (G = 1, 2, 4 or 8), by
+// DPP: a quad broadcast, and for G = 8 the other quad's copy through the
+// half-row mirror.
+template <int G, int S>
+__device__ __forceinline__ float group_bcast(float x, int g) {
+  static_assert(G <= 8 && S >= 0 && S < G, "group broadcast covers at most 8 lanes");
+  if constexpr (G == 1) {
+    return x;
+  } else {
+    constexpr int s = S & 3;
+    constexpr int sel = G == 2 ? (s | s << 2 | (2 + s) << 4 | (2 + s) << 6) : s * 0x55;
+    const int y = __builtin_amdgcn_update_dpp(0, __float_as_int(x), sel, 0xF, 0xF, false);
+    if constexpr (G <= 4) {
+      return __int_as_float(y);
+    } else {
+      const int m = __builtin_amdgcn_update_dpp(0, y, 0x141, 0xF, 0xF, false);
+      return __int_as_float(((g >> 2) == (S >> 2)) ? y : m);
+    }
+  }
 }
 
 // ------------------------------------------------------- partition walk --

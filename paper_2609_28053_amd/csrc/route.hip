@@ -26,6 +26,10 @@ namespace eqb {
 constexpr int kRmax = 16;              // extracted ranks kept per row
 constexpr int kList = 6;               // sorted keys kept per lane
 constexpr int kFastKmax = kRmax - 2;
+// Block of the fast kernel: 12 waves, three per SIMD, so that a wave may hold
+// up to 168 VGPRs (with 16 waves the cap of 128 forces spills).
+constexpr int kRouteBlock = 768;
+constexpr int kRouteWaves = kRouteBlock / 64;
 
 template <int E> struct FastCfg { static constexpr int G = E >= 64 ? 8 : E / 8; };
 
@@ -70,6 +74,46 @@ __device__ __forceinline__ V& at(B* base, uint32_t byte_off) {
   return *reinterpret_cast<V*>(reinterpret_cast<char*>(const_cast<std::remove_const_t<B>*>(base)) + byte_off);
 }
 
+// Coarse counts of the fast kernel for E >= 64: a slot-major packed
+// histogram.  Experts e, e+1 (e = 4j + 2h, a piece of four experts starting
+// at 4j and its half h) share a word, counted in its low and high 16 bits.
+// Half h lives in array h (64 KiB each); inside an array, slot 63 - j of bin
+// u is word u*64 + 63 - j.  The counter's byte offset h << 16 | u << 8 |
+// (252 - 4j) is assembled by one byte permute: u is the raw high byte of the
+// BF16 margin, 252 - 4j is byte 3 of the piece's index bytes (255 - e for
+// its four experts).  With the piece order rotated per row (below), the 64
+// lanes of a wave hit 64 different slots at E = 256, so 64 different LDS
+// banks.  Smaller E keep the expert-major layout of hist_row, which needs
+// less LDS.
+template <int E> constexpr bool kSlotHist = E >= 64;
+template <int E>
+constexpr int fast_hist_words() { return kSlotHist<E> ? 2 * 64 * kNBins : hist_words<E>(); }
+
+// Adds the coarse counts of a slot-major histogram to slab [E][256] (kappa
+// bins) and clears it.
+template <int E>
+__device__ __forceinline__ void flush_hist_slots(uint32_t* sh, int32_t* __restrict__ slab) {
+  for (int w = threadIdx.x; w < fast_hist_words<E>(); w += blockDim.x) {
+    const uint32_t c = sh[w];
+    if (c) {
+      const int e = 4 * (63 - (w & 63)) + 2 * (w >> 14);   // < E: no other slot is counted
+      const int bin = kappa_hi_of_raw((w >> 6) & 0xFF);
+      if (c & 0xFFFFu) atomicAdd(slab + e * kNBins + bin, (int32_t)(c & 0xFFFFu));
+      if (c >> 16) atomicAdd(slab + (e + 1) * kNBins + bin, (int32_t)(c >> 16));
+      sh[w] = 0;
+    }
+  }
+}
+
+// The histogram byte offset of half 1 of a piece: byte 3 of its index bytes
+// to byte 0, 1 to byte 2.  Volatile so that it is formed where it is used
+// rather than kept in a register per piece.
+__device__ __forceinline__ uint32_t half1_base(uint32_t ipk, uint32_t one16) {
+  uint32_t r;
+  asm volatile("v_perm_b32 %0, %1, %2, %3" : "=v"(r) : "v"(one16), "v"(ipk), "s"(0x0C060C03u));
+  return r;
+}
+
 // Insert key x into the sorted list L[0] >= ... >= L[n-1] (one max, n-1 med3).
 template <int n>
 __device__ __forceinline__ void list_insert(int (&L)[n], int x) {
@@ -79,7 +123,7 @@ __device__ __forceinline__ void list_insert(int (&L)[n], int x) {
 }
 
 template <int E, int KT>
-__global__ __launch_bounds__(kBlock) void route_fast_kernel(
+__global__ __launch_bounds__(kRouteBlock) void route_fast_kernel(
     const uint16_t* __restrict__ z, const float* __restrict__ b, int64_t T, int Kdyn,
     int32_t* __restrict__ topk_idx, float* __restrict__ topk_score, float* __restrict__ tau,
     int32_t* __restrict__ load, int32_t* __restrict__ hist, const PartTable pt,
@@ -88,38 +132,45 @@ __global__ __launch_bounds__(kBlock) void route_fast_kernel(
   constexpr int N = E / G;              // experts per lane
   constexpr int NQ = N / 4;             // 8-byte pieces per lane and row
   constexpr int R = 64 / G;             // rows per wave
-  constexpr int ROWS = kWaves * R;      // rows per block step
+  constexpr int ROWS = kRouteWaves * R;      // rows per block step
   constexpr int RSLOT = (kRmax + G - 1) / G;
   static_assert(N % 4 == 0 && N >= 8, "layout");
   static_assert(KT == 0 || KT + 2 <= E, "K+2 keys must exist");
   const int K = KT > 0 ? KT : Kdyn;
 
-  __shared__ uint32_t sh_hist[hist_words<E>()];
+  __shared__ uint32_t sh_hist[fast_hist_words<E>()];
   __shared__ uint32_t sh_load[E];
   __shared__ float sh_b[E];             // b as given: exact scores and tau
-  __shared__ float sh_bk[E];            // b with -0 as +0: the keys' sums
-  __shared__ uint2 sh_rank[kWaves][R][kRmax];   // (score bits, zbits << 16 | e) in rank order
+  __shared__ float sh_bk[NQ][E];        // b with -0 as +0 (the keys' sums), per piece rotation
+  __shared__ uint2 sh_rank[kRouteWaves][R][kRmax];   // (score bits, zbits << 16 | e) in rank order
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int g = lane % G, r = lane / G;
+  // Row r of a wave visits its pieces in the order q ^ rr, so at any step the
+  // rows of a wave work on different experts (distinct histogram slots).
+  const int rr = r & (NQ - 1);
 
-  // Piece q of this lane covers experts ex(q) .. ex(q)+3, so the G lanes of a
-  // row read 8*G contiguous bytes per piece.  b is read from LDS, four experts
-  // at a time (bias4: the keys' copy, bias4x: b as given).
-  auto ex = [&](int q) -> int { return q * 4 * G + g * 4; };
+  // Step q of this lane covers experts ex(q) .. ex(q)+3 (piece q ^ rr), so the
+  // G lanes of a row read 8*G contiguous bytes per step.  b is read from LDS,
+  // four experts at a time (bias4: the keys' copy, bias4x: b as given); the
+  // keys' copy is kept once per rotation, sh_bk[c][j] = b[j ^ 4Gc], so that a
+  // lane reads its step q at a fixed offset from its own base.
+  auto ex = [&](int q) -> int { return (q ^ rr) * 4 * G + g * 4; };
   // bytes 255 - e for the four experts of a piece (ex is a multiple of 4, no borrow)
   auto idxpk = [&](int q) -> uint32_t { return 0xFCFDFEFFu - (uint32_t)ex(q) * 0x01010101u; };
-  auto bias4 = [&](int q) -> float4 { return *reinterpret_cast<const float4*>(&sh_bk[ex(q)]); };
+  auto bias4 = [&](int q) -> float4 { return *reinterpret_cast<const float4*>(&sh_bk[rr][q * 4 * G + g * 4]); };
   auto bias4x = [&](int q) -> float4 { return *reinterpret_cast<const float4*>(&sh_b[ex(q)]); };
   auto pick = [](const float4& v, int i) -> float { return i == 0 ? v.x : i == 1 ? v.y : i == 2 ? v.z : v.w; };
 
-  for (int w = threadIdx.x; w < hist_words<E>(); w += kBlock) sh_hist[w] = 0;
+  for (int w = threadIdx.x; w < fast_hist_words<E>(); w += kRouteBlock) sh_hist[w] = 0;
   int fits = 1;
-  for (int e = threadIdx.x; e < E; e += kBlock) {
+  for (int e = threadIdx.x; e < E; e += kRouteBlock) {
     sh_load[e] = 0;
     const float bv = b[e];
     sh_b[e] = bv;
-    sh_bk[e] = (__float_as_uint(bv) == 0x80000000u) ? 0.0f : bv;
+    const float bk = (__float_as_uint(bv) == 0x80000000u) ? 0.0f : bv;
+#pragma unroll
+    for (int c = 0; c < NQ; ++c) sh_bk[c][e ^ (c * 4 * G)] = bk;
     fits &= (int)(fabsf(bv) < 0x1p119f);
   }
   // |z| <= 2^128 - 2^120 for a finite BF16 z, so with |b| < 2^119 every sum
@@ -161,7 +212,9 @@ __global__ __launch_bounds__(kBlock) void route_fast_kernel(
   float* seg_tau = tau;
 
   // t: row index inside the current segment
-  auto process = [&](const uint2 (&raw)[NQ], uint32_t t, bool valid) __attribute__((always_inline)) {
+  // raw holds this step's logits (loaded one step earlier); once they are
+  // widened, refill(raw) issues the next step's loads into the same registers.
+  auto process = [&](uint2 (&raw)[NQ], uint32_t t, bool valid, auto&& refill) __attribute__((always_inline)) {
     // ---- widen the logits once; build keys and the per-lane sorted list
     float zf[N];
 #pragma unroll
@@ -171,6 +224,7 @@ __global__ __launch_bounds__(kBlock) void route_fast_kernel(
       zf[q * 4 + 2] = bf16_lo(raw[q].y);
       zf[q * 4 + 3] = bf16_hi(raw[q].y);
     }
+    refill(raw);
     int L[kList];
 #pragma unroll
     for (int j = 0; j < kList; ++j) L[j] = kKeyNone;
@@ -226,7 +280,7 @@ __global__ __launch_bounds__(kBlock) void route_fast_kernel(
           // below E for every key of the row; the clamp keeps a row whose
           // keys cannot be trusted (it goes slow) inside its own logits
           e = min(255 - (rk[s] & 0xFF), E - 1);
-          zc = z_from_key(rk[s], sh_bk[e], &ok);
+          zc = z_from_key(rk[s], sh_bk[0][e], &ok);
         }
         zown[s] = z_or_load(zc, ok, &at<uint16_t>(seg_z, (t * E + e) * 2u));
       }
@@ -276,7 +330,7 @@ __global__ __launch_bounds__(kBlock) void route_fast_kernel(
             const int key = (int)myrank[k].x;
             const int e = 255 - (key & 0xFF);
             bool ok;
-            uint32_t zb = z_from_key(key, sh_bk[e], &ok);
+            uint32_t zb = z_from_key(key, sh_bk[0][e], &ok);
             if (!ok) zb = seg_z[t * E + e];
             const uint32_t sb = __float_as_uint(__uint_as_float(zb << 16) + sh_b[e]);
             myrank[k] = make_uint2(sb, (zb << 16) | (uint32_t)e);
@@ -405,10 +459,9 @@ __global__ __launch_bounds__(kBlock) void route_fast_kernel(
       }
       tv = tk;
     }
-    if (KT > 0) {
+    if constexpr (KT > 0) {
       // every lane of the row takes tau from the lane holding rank K
-      const int src = (lane - g) + (K % G);
-      tv = __shfl(tv, src);
+      tv = group_bcast<G, KT % G>(tv, g);
     }
     if (valid && fromlds) {
 #pragma unroll
@@ -430,12 +483,25 @@ __global__ __launch_bounds__(kBlock) void route_fast_kernel(
     if (hist && valid) {
 #pragma unroll
       for (int q = 0; q < NQ; ++q) {
-        const uint32_t row = hist_row(ex(q));
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
           const uint32_t p = bf16x2_bits(tv - zf[q * 4 + 2 * h], tv - zf[q * 4 + 2 * h + 1]);
-          atomicAdd(&sh_hist[row + h * kHistStride + ((p >> 8) & 0xFFu)], 1u);
-          atomicAdd(&sh_hist[row + h * kHistStride + (p >> 24)], 1u << 16);
+          if constexpr (kSlotHist<E>) {
+            // byte offsets: the raw high byte of either margin becomes byte 1
+            if (h == 0) {
+              const uint32_t ipk = idxpk(q);
+              atomicAdd(&at<uint32_t>(sh_hist, __builtin_amdgcn_perm(ipk, p, 0x0C0C0107u)), 1u);
+              atomicAdd(&at<uint32_t>(sh_hist, __builtin_amdgcn_perm(ipk, p, 0x0C0C0307u)), 1u << 16);
+            } else {
+              const uint32_t base = half1_base(idxpk(q), 0x10000u);
+              atomicAdd(&at<uint32_t>(sh_hist, __builtin_amdgcn_perm(base, p, 0x0C060104u)), 1u);
+              atomicAdd(&at<uint32_t>(sh_hist, __builtin_amdgcn_perm(base, p, 0x0C060304u)), 1u << 16);
+            }
+          } else {
+            const uint32_t row = hist_row(ex(q)) + h * kHistStride;
+            atomicAdd(&sh_hist[row + ((p >> 8) & 0xFFu)], 1u);
+            atomicAdd(&sh_hist[row + (p >> 24)], 1u << 16);
+          }
         }
       }
     }
@@ -443,7 +509,7 @@ __global__ __launch_bounds__(kBlock) void route_fast_kernel(
   };
 
   for_each_segment(r0, r1, pt, [&](int p, int64_t s0, int64_t s1) {
-    uint2 bufa[NQ], bufb[NQ];
+    uint2 buf[NQ];
     // a row past the segment reads the segment's last row; it is processed
     // as invalid (no output, no count)
     seg_z = z + s0 * E;
@@ -454,26 +520,30 @@ __global__ __launch_bounds__(kBlock) void route_fast_kernel(
     auto load_rows = [&](uint2* dst, uint32_t base) {
       uint32_t t = base + wave * R + r;
       t = t < n ? t : n - 1;
-      const uint32_t off = (t * (uint32_t)E + (uint32_t)g * 4u) * 2u;    // bytes, < 2^25
+      // bytes, < 2^25; the piece index occupies bits that the row and lane
+      // parts leave clear, so XOR selects piece q ^ rr
+      const uint32_t off = (t * (uint32_t)E + (uint32_t)g * 4u) * 2u + (uint32_t)rr * (8u * G);
 #pragma unroll
-      for (int q = 0; q < NQ; ++q) dst[q] = at<uint2>(seg_z, off + (uint32_t)q * (8u * G));
+      for (int q = 0; q < NQ; ++q) dst[q] = at<uint2>(seg_z, off ^ ((uint32_t)q * (8u * G)));
     };
-    // The next step's loads are in flight while a step is processed.  Each
-    // step starts by taking the rows prefetched one step earlier, so no load
-    // is still pending in the registers a step works on and the only wait is
-    // for loads issued a whole step before.
-    load_rows(bufb, 0);
+    // The next step's loads are in flight while a step is processed: a step
+    // widens the rows loaded one step earlier and then reuses their registers
+    // for the next step's loads, so the only wait is for loads issued a whole
+    // step before.
+    load_rows(buf, 0);
     for (uint32_t base = 0; base < n; base += ROWS) {
-#pragma unroll
-      for (int q = 0; q < NQ; ++q) bufa[q] = bufb[q];
-      if (base + ROWS < n) load_rows(bufb, base + ROWS);
       const uint32_t t = base + wave * R + r;
-      process(bufa, t, t < n);
+      process(buf, t, t < n, [&](uint2 (&dst)[NQ]) {
+        if (base + ROWS < n) load_rows(dst, base + ROWS);
+      });
     }
     __syncthreads();
-    if (hist) flush_hist<E, false>(sh_hist, hist + (int64_t)p * E * kNBins, nullptr);
+    if (hist) {
+      if constexpr (kSlotHist<E>) flush_hist_slots<E>(sh_hist, hist + (int64_t)p * E * kNBins);
+      else flush_hist<E, false>(sh_hist, hist + (int64_t)p * E * kNBins, nullptr);
+    }
     if (load) {
-      for (int e = threadIdx.x; e < E; e += kBlock) {
+      for (int e = threadIdx.x; e < E; e += kRouteBlock) {
         const uint32_t c = sh_load[e];
         if (c) atomicAdd(&load[(int64_t)p * E + e], (int32_t)c);
         sh_load[e] = 0;
@@ -566,8 +636,8 @@ template <int E, int KT>
 void launch_fast(const RouteArgs& a, hipStream_t s) {
   int blocks;
   int64_t rpb;
-  grid_for(a.T, kWaves * (64 / FastCfg<E>::G), 1, &blocks, &rpb);
-  route_fast_kernel<E, KT><<<blocks, kBlock, 0, s>>>(a.z, a.b, a.T, a.K, a.idx, a.score, a.tau, a.load,
+  grid_for(a.T, kRouteWaves * (64 / FastCfg<E>::G), 1, &blocks, &rpb);
+  route_fast_kernel<E, KT><<<blocks, kRouteBlock, 0, s>>>(a.z, a.b, a.T, a.K, a.idx, a.score, a.tau, a.load,
                                                      a.hist, a.pt, rpb);
 }
 
