@@ -218,6 +218,41 @@ __device__ __forceinline__ float group_bcast(float x, int g) {
   }
 }
 
+// ------------------------------------------------ per-expert selection --
+// Inclusive scan of one count per thread over a 256-thread block: a scan
+// inside each wave, then the totals of the lower waves.  Counts and their
+// sums stay below 2^31 (T < 2^31).
+__device__ __forceinline__ int64_t block_inclusive_scan_256(int64_t x64, int64_t* sh) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  int x = (int)x64;
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    const int y = __shfl_up(x, d);
+    if (lane >= d) x += y;
+  }
+  if (lane == 63) sh[wave] = x;
+  __syncthreads();
+  int lower = 0;
+  for (int w = 0; w < wave; ++w) lower += (int)sh[w];
+  return (int64_t)(x + lower);
+}
+
+// Sum over the P slabs of one counter; the loads are issued eight at a time
+// so that their latencies overlap.
+__device__ __forceinline__ int64_t slab_sum(const int32_t* __restrict__ hist, int P, int64_t stride) {
+  int64_t c = 0;
+  int q = 0;
+  for (; q + 8 <= P; q += 8) {
+    int v[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) v[j] = hist[(q + j) * stride];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) c += v[j];
+  }
+  for (; q < P; ++q) c += hist[q * stride];
+  return c;
+}
+
 // ------------------------------------------------------- partition walk --
 // Calls f(p, s0, s1) for every piece of [r0, r1) lying in one partition and
 // holding at most kSegMax rows.  Uniform across the block.

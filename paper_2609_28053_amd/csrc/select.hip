@@ -6,20 +6,6 @@
 
 namespace eqb {
 
-// Inclusive scan of one value per thread over a 256-thread block.
-__device__ __forceinline__ int64_t block_inclusive_scan_256(int64_t x, int64_t* sh) {
-  const int i = threadIdx.x;
-  sh[i] = x;
-  __syncthreads();
-  for (int d = 1; d < kNBins; d <<= 1) {
-    const int64_t add = (i >= d) ? sh[i - d] : 0;
-    __syncthreads();
-    sh[i] += add;
-    __syncthreads();
-  }
-  return sh[i];
-}
-
 // One block per expert (and, with kLocal, per partition), one thread per bin.
 // Global: the P slabs are summed first (the all-reduce) and r is the rank over
 // the whole batch.  kLocal: slab p alone, with its own rank
@@ -48,7 +34,7 @@ __global__ __launch_bounds__(kNBins) void select_coarse_kernel(
   if (kLocal) {
     c = hist[((int64_t)p * E + e) * kNBins + u];
   } else {
-    for (int q = 0; q < P; ++q) c += hist[((int64_t)q * E + e) * kNBins + u];
+    c = slab_sum(hist + (int64_t)e * kNBins + u, P, (int64_t)E * kNBins);
     if (hist_sum) hist_sum[(int64_t)e * kNBins + u] = (int32_t)c;
   }
   const int64_t cum = block_inclusive_scan_256(c, sh);
@@ -82,7 +68,7 @@ __global__ __launch_bounds__(kNBins) void select_fine_kernel(
   if (kLocal) {
     c = hist[((int64_t)p * E + e) * kNBins + v];
   } else {
-    for (int q = 0; q < P; ++q) c += hist[((int64_t)q * E + e) * kNBins + v];
+    c = slab_sum(hist + (int64_t)e * kNBins + v, P, (int64_t)E * kNBins);
     if (hist_sum) hist_sum[(int64_t)e * kNBins + v] = (int32_t)c;
   }
   const int64_t cum = block_inclusive_scan_256(c, sh);

@@ -145,18 +145,8 @@ __global__ __launch_bounds__(kNBins) void select_uniform_kernel(
     double* __restrict__ est, int32_t* __restrict__ status) {
   __shared__ int64_t sh[kNBins];
   const int e = blockIdx.x, j = threadIdx.x;
-  int64_t c = 0;
-  if (j < nbins)
-    for (int p = 0; p < P; ++p) c += hist[((int64_t)p * E + e) * nbins + j];
-  sh[j] = c;
-  __syncthreads();
-  for (int d = 1; d < kNBins; d <<= 1) {
-    const int64_t add = (j >= d) ? sh[j - d] : 0;
-    __syncthreads();
-    sh[j] += add;
-    __syncthreads();
-  }
-  const int64_t cum = sh[j];
+  const int64_t c = (j < nbins) ? slab_sum(hist + (int64_t)e * nbins + j, P, (int64_t)E * nbins) : 0;
+  const int64_t cum = block_inclusive_scan_256(c, sh);
   if (c > 0 && cum >= r && cum - c < r)
     est[e] = lo + ((double)j + (double)(r - (cum - c)) / (double)c) * width;
   if (j == kNBins - 1 && cum < r) {
