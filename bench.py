@@ -254,8 +254,8 @@ def variants_leg(w, eqb, torch, zt, bt, lay, part_off):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="large256")
     ap.add_argument("--cpu-rows", type=int, default=1048576,
                     help="tokens in the CPU-oracle baseline slice (0 disables it)")
