@@ -299,9 +299,12 @@ def main():
     stream = torch.cuda.Stream(device=dev)     # default priority
     lay = eqb.Layer(w.T, w.E, w.K, w.P, device=dev)
 
-    def step(ev=None, zin=None):
+    def step(ev=None, zin=None, marks=range(6)):
+        """One layer step; ev[i] is recorded at point i for i in marks
+        (0 start, 1 after zeroing, 2 after route, 3 after select 1,
+        4 after pass 2, 5 end)."""
         zin = zt if zin is None else zin
-        rec = (lambda i: ev[i].record(stream)) if ev else (lambda i: None)
+        rec = (lambda i: ev[i].record(stream) if i in marks else None) if ev else (lambda i: None)
         rec(0)
         lay._counts.zero_()
         rec(1)
@@ -321,27 +324,38 @@ def main():
     with torch.cuda.stream(stream):
         for _ in range(args.warmup):
             step()
-        # per-kernel durations come from HIP events recorded on the launch stream
+        # Timed region: exactly `steps` steps.  The only events recorded in it
+        # bracket the route kernel on its launch stream (its live duration for
+        # the roofline); an event between every stage would itself add a few
+        # microseconds per step.
         evs = [[torch.cuda.Event(enable_timing=True) for _ in range(6)] for _ in range(args.steps)]
         torch.cuda.synchronize()
         t0 = time.perf_counter()
-        for i in range(args.steps):            # timed region: exactly `steps` steps
-            step(evs[i])
+        for i in range(args.steps):
+            step(evs[i], marks=(1, 2))
         torch.cuda.synchronize()
         elapsed = time.perf_counter() - t0
+        # Stage breakdown: a separate run of steps with an event after every stage.
+        n_stage = min(args.steps, 20)
+        sevs = [[torch.cuda.Event(enable_timing=True) for _ in range(6)] for _ in range(n_stage)]
+        for i in range(n_stage):
+            step(sevs[i])
+        torch.cuda.synchronize()
     assert int(lay.dev_status.item()) == 0, "device reported a rank beyond the counts"
 
     names = ["zero", "route_hist1", "select1", "margin_hist2", "select2"]
-    stage_ms = {n: float(np.mean([evs[i][j].elapsed_time(evs[i][j + 1]) for i in range(args.steps)]))
+    stage_ms = {n: float(np.mean([sevs[i][j].elapsed_time(sevs[i][j + 1]) for i in range(n_stage)]))
                 for j, n in enumerate(names)}
+    route_ms = float(np.mean([evs[i][1].elapsed_time(evs[i][2]) for i in range(args.steps)]))
     ms_per_step = elapsed * 1e3 / args.steps
-    per_step = np.array([evs[i][0].elapsed_time(evs[i][5]) for i in range(args.steps)])
+    per_step = np.array([sevs[i][0].elapsed_time(sevs[i][5]) for i in range(n_stage)])
     step_ms = {"median": float(np.median(per_step)), "min": float(per_step.min()),
-               "p90": float(np.percentile(per_step, 90))}
+               "p90": float(np.percentile(per_step, 90)), "steps": n_stage,
+               "note": "a separate run with an event after every stage"}
     tokens_per_s = w.T / (ms_per_step * 1e-3)
     pass_gbs = pass_bytes_per_token(w.E, w.K) * w.T / (ms_per_step * 1e-3) / 1e9
     route_bytes = route_bytes_per_token(w.E, w.K) * w.T
-    route_gbs = route_bytes / (stage_ms["route_hist1"] * 1e-3) / 1e9
+    route_gbs = route_bytes / (route_ms * 1e-3) / 1e9
     traffic = read_traffic(w.T)
     # The route kernel is limited by vector instruction issue, not by HBM:
     # its issued VALU (counted offline) over its live duration, against the
@@ -350,7 +364,7 @@ def main():
     valu_view = None
     if vpe is not None:
         ops = vpe * w.T * w.E
-        achieved = ops / (stage_ms["route_hist1"] * 1e-3)
+        achieved = ops / (route_ms * 1e-3)
         valu_view = {"valu_per_element": vpe, "achieved_lane_ops_per_s": achieved,
                      "peak_lane_ops_per_s": VALU_PEAK_LANE_OPS, "frac": achieved / VALU_PEAK_LANE_OPS,
                      "source": os.path.relpath(VALU_FILE, ROOT)}
@@ -375,7 +389,7 @@ def main():
         "pass_frac_of_peak": pass_gbs / HBM_PEAK_GBS,
         "stage_ms": stage_ms,
         "step_ms_events": step_ms,
-        "roofline": {"kernel": "route_hist1", "bound": "hbm", "achieved": route_gbs,
+        "roofline": {"kernel": "route_hist1", "bound": "hbm", "achieved": route_gbs, "launch_ms": route_ms,
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": route_gbs / HBM_PEAK_GBS,
                      "traffic": traffic, "algorithmic_bytes": route_bytes,
                      "valu_issue": valu_view},
