@@ -41,28 +41,16 @@ template <int E> struct FastCfg { static constexpr int G = E >= 64 ? 8 : E / 8; 
 // fl32(z + b) is checked to reproduce H.  The two zeros are the exception:
 // +0 and -0 give the same sum, and which one z is decides the sign of a zero
 // tau, so a zero is never accepted.  *ok reports the check; otherwise z must
-// be read from memory (z_or_load).
+// be read from memory.
 __device__ __forceinline__ uint32_t z_from_key(int key, float b, bool* ok) {
   const uint32_t kb = (uint32_t)key;
   const float s_mid = __uint_as_float((kb & 0xFFFFFF00u) | 0x80u);
   const uint32_t zc = bf16x2_bits(s_mid - b, 0.0f) & 0xFFFFu;
   const uint32_t sc = __float_as_uint(__uint_as_float(zc << 16) + b);
   const int ez = (int)((zc >> 7) & 0xFFu), es = (int)((kb >> 23) & 0xFFu);
-  *ok = ((sc ^ kb) < 256u) && (ez >= es - 6) && ((zc & 0x7F80u) != 0x7F80u) && ((zc & 0x7FFFu) != 0u);
-  return zc;
-}
-
-// Replaces the recovered z by the stored one where the recovery failed.  The
-// load and its use sit inside a branch the whole wave takes or skips, so the
-// common case carries no pending load (and no wait that would also drain the
-// prefetched rows).
-__device__ __forceinline__ uint32_t z_or_load(uint32_t zc, bool ok, const uint16_t* zptr) {
-  if (__builtin_expect(__any(!ok), 0)) {
-    uint32_t zl = zc;
-    if (!ok) zl = *zptr;
-    zc = zl | 0u;
-    __builtin_amdgcn_s_waitcnt(0);
-  }
+  // bitwise, not short-circuit: the four tests are cheap and a branch per
+  // test would cost more than they do
+  *ok = ((sc ^ kb) < 256u) & (ez >= es - 6) & ((zc & 0x7F80u) != 0x7F80u) & ((zc & 0x7FFFu) != 0u);
   return zc;
 }
 
@@ -269,20 +257,37 @@ __global__ __launch_bounds__(kRouteBlock) void route_fast_kernel(
         if (k == KT) mK = M;
         if (k == KT + 1) mK1 = M;
       }
-      // z of the experts at this lane's ranks, recovered from their keys
+      // z of the experts at this lane's ranks, recovered from their keys.
+      // Every slot's bias is read before any is used, so the LDS latency is
+      // paid once; one wave-wide test sends the failed recoveries to memory.
+      int es[RSLOT];
+      bool use[RSLOT], ok[RSLOT];
+      float bks[RSLOT];
 #pragma unroll
       for (int s = 0; s < RSLOT; ++s) {
-        const int k = s * G + g;
-        bool ok = true;
-        uint32_t zc = 0;
-        int e = 0;
-        if (valid && k <= KT) {
-          // below E for every key of the row; the clamp keeps a row whose
-          // keys cannot be trusted (it goes slow) inside its own logits
-          e = min(255 - (rk[s] & 0xFF), E - 1);
-          zc = z_from_key(rk[s], sh_bk[0][e], &ok);
+        use[s] = valid && s * G + g <= KT;
+        // below E for every key of the row; the clamp keeps a row whose
+        // keys cannot be trusted (it goes slow) inside its own logits
+        es[s] = use[s] ? min(255 - (rk[s] & 0xFF), E - 1) : 0;
+        bks[s] = sh_bk[0][es[s]];
+      }
+      bool bad = false;
+#pragma unroll
+      for (int s = 0; s < RSLOT; ++s) {
+        zown[s] = z_from_key(rk[s], bks[s], &ok[s]);
+        ok[s] = ok[s] | !use[s];
+        bad = bad | !ok[s];
+      }
+      if (__builtin_expect(__any(bad), 0)) {
+        // the loads and their use stay inside a branch the whole wave takes
+        // or skips, so the common case carries no pending load
+#pragma unroll
+        for (int s = 0; s < RSLOT; ++s) {
+          uint32_t zl = zown[s];
+          if (!ok[s]) zl = at<uint16_t>(seg_z, (t * E + es[s]) * 2u);
+          zown[s] = zl | 0u;
         }
-        zown[s] = z_or_load(zc, ok, &at<uint16_t>(seg_z, (t * E + e) * 2u));
+        __builtin_amdgcn_s_waitcnt(0);
       }
       const int tauhi = mK >> 8;
       const bool dry = group_max_i32<G>((int)(L[0] == kKeyNone)) != 0;
