@@ -3,14 +3,19 @@
 // 2609.28053, Sec. 2 Eq. 1, "Quantile Balancing", Appendix C).
 //
 // Fast kernel (K <= kFastKmax).  A row of E logits is spread over G lanes,
-// each holding N = E/G experts as N/4 8-byte pieces.  Per element it forms a
+// each holding N = E/G experts as N/4 8-byte pieces; row r of a wave visits
+// its pieces in the order q XOR r, so that at any step the rows of a wave
+// work on different experts (and count into different LDS words).  The
+// coarse counts, two margins per BF16 conversion, go to a slot-major LDS
+// histogram addressed by one byte permute.  Per element the kernel forms a
 // 32-bit key: the binary32 bits of s = z + b with the low byte replaced by
 // 255 - e, and keeps a sorted list of its kList largest keys (one maximum and
 // kList-1 medians per element).  Keys are compared as floats, so negative
 // scores order correctly; the key's sum takes -0 in b as +0, so a score of
 // -0 keys as +0 and the two zeros share one run of keys.
 // K+2 extraction rounds then take the group maximum of the list heads with
-// DPP and pop the winner, refilling a lane whose list runs dry.  Key order is
+// DPP and pop the winner (the generic-K variant refills a lane whose list
+// runs dry; the unrolled variants send such rows to the exact path).  Key order is
 // score order except between scores that agree in their top 24 bits;
 // extraction continues until the last key leaves the top-24-bit run of rank
 // K, the winners' exact scores are recomputed from z and b, and a row whose
