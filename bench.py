@@ -211,6 +211,33 @@ def signs_leg(torch, zt, lay, run_step, reps=10, shift=4.0):
             "step_ms_median": float(np.median([e[0].elapsed_time(e[5]) for e in evs]))}
 
 
+def per_rank_leg(eqb, torch, stream, steps=200):
+    """The whole step at one data-parallel rank's share of the paper's
+    training step (rank256: 147,456 tokens of E = 256, K = 6, App. E),
+    timed on the wall clock over `steps` steps like the main measurement."""
+    import workloads as W
+    w = W.WORKLOADS["rank256"]
+    z, b, off = W.generate(w)
+    dev = torch.device("cuda:0")
+    zt = torch.from_numpy(z.view(np.int16)).to(dev)
+    bt = torch.from_numpy(b).to(dev)
+    part_off = [int(x) for x in off]
+    lay = eqb.Layer(w.T, w.E, w.K, w.P, device=dev)
+    with torch.cuda.stream(stream):
+        for _ in range(10):
+            lay.run(zt, bt, part_off, stream=stream)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(steps):
+            lay.run(zt, bt, part_off, stream=stream)
+        torch.cuda.synchronize()
+        ms = (time.perf_counter() - t0) * 1e3 / steps
+    gbs = pass_bytes_per_token(w.E, w.K) * w.T / (ms * 1e-3) / 1e9
+    return {"workload": w.name, "T": w.T, "E": w.E, "K": w.K, "steps": steps, "ms_per_step": ms,
+            "tokens_per_s": w.T / (ms * 1e-3), "pass_hbm_gbs": gbs, "pass_frac_of_peak": gbs / HBM_PEAK_GBS,
+            "note": "z is 72 MiB here, so part of it can be served from the 256 MB memory-side cache"}
+
+
 def variants_leg(w, eqb, torch, zt, bt, lay, part_off):
     """The statistics EQB is compared with (Sec. 2), on the same batch: the
     rank-averaged quantile (P shards, and P/4 shards to show that it depends
@@ -399,6 +426,7 @@ def main():
         out["variants"] = variants_leg(w, eqb, torch, zt, bt, lay, part_off)
         with torch.cuda.stream(stream):
             out["cutoff_signs"] = signs_leg(torch, zt, lay, step)
+        out["per_rank"] = per_rank_leg(eqb, torch, stream)
     if args.qb_steps > 0:
         del zt
         out["qb_loop"] = qb_loop_leg(w, eqb, torch, args.qb_steps, dev, part_off)

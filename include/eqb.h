@@ -29,7 +29,10 @@
  *   (empty partitions are allowed).  part_off = NULL means P = 1.  Summing the
  *   slabs over p is the all-reduce of Algorithm 1, steps 2 and 5.
  * Accumulation.  Histogram and load outputs are ACCUMULATED (+=): zero them
- *   before the first call of a layer.
+ *   before the first call of a layer.  Every count must stay in [0, 2^31)
+ *   before and after a call: the kernels may add to two adjacent int32
+ *   counters with one 64-bit atomic, which is exact only while no counter
+ *   wraps.  Counts are token counts, so T < 2^31 keeps them in range.
  * Numerics.  z + b and tau - z are single binary32 operations rounded to
  *   nearest even, with subnormals kept; a margin is rounded once to BF16
  *   (nearest, ties to even).  kappa(bits) = bits ^ (sign ? 0xFFFF : 0x8000),

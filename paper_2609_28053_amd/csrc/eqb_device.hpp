@@ -290,29 +290,76 @@ __device__ __forceinline__ void for_each_segment_rev(int64_t r0, int64_t r1, con
 template <int E>
 constexpr int hist_words() { return (E / 2) * kHistStride; }
 
+// Flush order: the i-th word a block visits when it adds its LDS counts to
+// global memory.  Blocks start at different words (a stride per block that
+// is not a multiple of the bank count), so that blocks flushing at the same
+// time add to different global counters instead of queueing on one address.
+__device__ __forceinline__ int flush_word(int i, int nwords) {
+  int w = i + (int)((blockIdx.x * 1031u) % (uint32_t)nwords);
+  return w >= nwords ? w - nwords : w;
+}
+
+// Adds n_lo to counter c[0] and n_hi to c[1] (two adjacent int32 counters):
+// one 64-bit atomic when c is 8-byte aligned, else two 32-bit ones.  The
+// 64-bit add is exact because no count reaches 2^31, so the low word never
+// carries into the high one.
+__device__ __forceinline__ void add_count_pair(int32_t* c, uint32_t n_lo, uint32_t n_hi) {
+  if ((reinterpret_cast<uintptr_t>(c) & 7u) == 0) {
+    atomicAdd(reinterpret_cast<unsigned long long*>(c),
+              (unsigned long long)n_lo | ((unsigned long long)n_hi << 32));
+  } else {
+    if (n_lo) atomicAdd(c, (int32_t)n_lo);
+    if (n_hi) atomicAdd(c + 1, (int32_t)n_hi);
+  }
+}
+
+// Adds the counts of raw bins 2j (n_even) and 2j+1 (n_odd) of expert e to
+// its row of kappa bins.  Both raw bins of a pair map to two adjacent kappa
+// bins: in order when the map keeps the low bit (XOR 0x80, or no change for
+// a fine bin of a non-negative selection), swapped when it flips every bit
+// (XOR 0xFF).
+__device__ __forceinline__ void add_raw_pair(int32_t* row, bool flips, uint32_t n_even, uint32_t n_odd,
+                                             int kappa_even) {
+  if (!flips) add_count_pair(row + kappa_even, n_even, n_odd);
+  else add_count_pair(row + (kappa_even - 1), n_odd, n_even);
+}
+
+// Adds a block's packed LDS counts to global slab [E][256] (kappa bins) and
+// clears them, one pair of adjacent raw bins per thread and step.
 // kFine = false: raw high byte -> kappa high byte (same map for every expert).
 // kFine = true : raw low byte  -> kappa low byte, flipped for experts whose
-//                selected coarse bin holds negative values (u_e < 0x80).
+//                selected coarse bin holds negative values (u_e < 0x80);
+//                experts without a valid selection are skipped.
 template <int E, bool kFine>
 __device__ __forceinline__ void flush_hist(uint32_t* sh, int32_t* __restrict__ slab,
                                            const int32_t* __restrict__ sel_hi) {
-  for (int w = threadIdx.x; w < hist_words<E>(); w += blockDim.x) {
-    const uint32_t c = sh[w];
-    if (c) {
-      const int pair = w / kHistStride;
-      const int raw = w - pair * kHistStride;
+  constexpr int kItems = (E / 2) * (kNBins / 2);
+  for (int i = threadIdx.x; i < kItems; i += blockDim.x) {
+    const int it = flush_word(i, kItems);
+    const int pair = it / (kNBins / 2), j = it % (kNBins / 2);
+    const int w0 = pair * kHistStride + 2 * j;
+    const uint32_t c0 = sh[w0], c1 = sh[w0 + 1];
+    if (c0 | c1) {
 #pragma unroll
       for (int h = 0; h < 2; ++h) {
-        const uint32_t n = h ? (c >> 16) : (c & 0xFFFFu);
-        if (n) {
-          const int e = 2 * pair + h;
-          int bin;
-          if (kFine) bin = (sel_hi[e] < 0x80) ? (raw ^ 0xFF) : raw;
-          else bin = kappa_hi_of_raw(raw);
-          atomicAdd(slab + e * kNBins + bin, (int32_t)n);
+        const uint32_t n0 = h ? (c0 >> 16) : (c0 & 0xFFFFu);
+        const uint32_t n1 = h ? (c1 >> 16) : (c1 & 0xFFFFu);
+        const int e = 2 * pair + h;
+        if (n0 | n1) {
+          if (kFine) {
+            const int u = sel_hi[e];
+            if (u >= 0 && u < kNBins) {
+              const bool neg = u < 0x80;
+              add_raw_pair(slab + e * kNBins, neg, n0, n1, neg ? (2 * j) ^ 0xFF : 2 * j);
+            }
+          } else {
+            const bool neg = (2 * j) & 0x80;
+            add_raw_pair(slab + e * kNBins, neg, n0, n1, kappa_hi_of_raw(2 * j));
+          }
         }
       }
-      sh[w] = 0;
+      sh[w0] = 0;
+      sh[w0 + 1] = 0;
     }
   }
 }

@@ -116,23 +116,7 @@ __global__ __launch_bounds__(kBlock) void margin_hist_kernel(
     if (!kFine) {
       flush_hist<E, false>(sh_hist, slab, nullptr);
     } else {
-      // skip experts whose selection is invalid
-      for (int w = threadIdx.x; w < hist_words<E>(); w += kBlock) {
-        const uint32_t c = sh_hist[w];
-        if (c) {
-          const int pair = w / kHistStride;
-          const int lr = w - pair * kHistStride;
-#pragma unroll
-          for (int h = 0; h < 2; ++h) {
-            const uint32_t n = h ? (c >> 16) : (c & 0xFFFFu);
-            const int e = 2 * pair + h;
-            const int u = sel[e];
-            if (n && u >= 0 && u < kNBins)
-              atomicAdd(slab + e * kNBins + ((u < 0x80) ? (lr ^ 0xFF) : lr), (int32_t)n);
-          }
-          sh_hist[w] = 0;
-        }
-      }
+      flush_hist<E, true>(sh_hist, slab, sel);
     }
     __syncthreads();
   });

@@ -83,17 +83,24 @@ template <int E>
 constexpr int fast_hist_words() { return kSlotHist<E> ? 2 * 64 * kNBins : hist_words<E>(); }
 
 // Adds the coarse counts of a slot-major histogram to slab [E][256] (kappa
-// bins) and clears it.
+// bins) and clears it, one pair of adjacent raw bins (words 64 apart) per
+// thread and step.
 template <int E>
 __device__ __forceinline__ void flush_hist_slots(uint32_t* sh, int32_t* __restrict__ slab) {
-  for (int w = threadIdx.x; w < fast_hist_words<E>(); w += blockDim.x) {
-    const uint32_t c = sh[w];
-    if (c) {
-      const int e = 4 * (63 - (w & 63)) + 2 * (w >> 14);   // < E: no other slot is counted
-      const int bin = kappa_hi_of_raw((w >> 6) & 0xFF);
-      if (c & 0xFFFFu) atomicAdd(slab + e * kNBins + bin, (int32_t)(c & 0xFFFFu));
-      if (c >> 16) atomicAdd(slab + (e + 1) * kNBins + bin, (int32_t)(c >> 16));
-      sh[w] = 0;
+  constexpr int kItems = fast_hist_words<E>() / 2;
+  for (int i = threadIdx.x; i < kItems; i += blockDim.x) {
+    const int it = flush_word(i, kItems);
+    const int arr = it >> 13, j = (it >> 6) & 127, slot = it & 63;
+    const int w0 = arr * 16384 + 2 * j * 64 + slot;
+    const uint32_t c0 = sh[w0], c1 = sh[w0 + 64];
+    if (c0 | c1) {
+      const int e = 4 * (63 - slot) + 2 * arr;   // < E: no other slot is counted
+      const bool neg = (2 * j) & 0x80;
+      const int k0 = kappa_hi_of_raw(2 * j);
+      if ((c0 | c1) & 0xFFFFu) add_raw_pair(slab + e * kNBins, neg, c0 & 0xFFFFu, c1 & 0xFFFFu, k0);
+      if ((c0 | c1) >> 16) add_raw_pair(slab + (e + 1) * kNBins, neg, c0 >> 16, c1 >> 16, k0);
+      sh[w0] = 0;
+      sh[w0 + 64] = 0;
     }
   }
 }
