@@ -257,18 +257,25 @@ __global__ __launch_bounds__(kRouteBlock) void route_fast_kernel(
     }
 
     if constexpr (KT > 0) {
-      int mK = kKeyNone, mK1 = kKeyNone, prev = kKeyNone;
+      int mK = kKeyNone, prev = kKeyNone;
       bool near = false;      // two adjacent extracted keys share their top 24 bits
 #pragma unroll
-      for (int k = 0; k < KT + 2; ++k) {
+      for (int k = 0; k <= KT; ++k) {
         const int M = group_max_key<G>(L[0]);
-        if (k < KT + 1) pop(M);
+        pop(M);
         rk[k / G] = (g == k % G) ? M : rk[k / G];
         if (k > 0) near |= ((uint32_t)(M ^ prev) < 256u);
         prev = M;
         if (k == KT) mK = M;
-        if (k == KT + 1) mK1 = M;
       }
+      // Rank K+1 is the largest list head left.  Whether it shares the top 24
+      // bits of rank K, and whether a list ran dry, are read off the heads
+      // directly; the rest of each list is not needed past this point (a row
+      // that extends its run rebuilds its lists), so the last rounds' pops
+      // only shift the entries that later rounds read.  A dry head (-inf)
+      // never matches: no finite key has the top 24 bits of -inf.
+      const int head = ((uint32_t)(L[0] ^ mK) < 256u) ? 1 : 0;
+      const int rowflag = group_max_i32<G>(L[0] == kKeyNone ? 2 : head);
       // z of the experts at this lane's ranks, recovered from their keys.
       // Every slot's bias is read before any is used, so the LDS latency is
       // paid once; one wave-wide test sends the failed recoveries to memory.
@@ -302,24 +309,24 @@ __global__ __launch_bounds__(kRouteBlock) void route_fast_kernel(
         __builtin_amdgcn_s_waitcnt(0);
       }
       const int tauhi = mK >> 8;
-      const bool dry = group_max_i32<G>((int)(L[0] == kKeyNone)) != 0;
+      const bool dry = rowflag == 2;
       slow = valid && !bias_ok;
-      staged = valid && !slow && (near || dry);
-      nrank = KT + 2;
+      staged = valid && !slow && (near || rowflag != 0);
+      nrank = KT + 1;
       if (__any(staged)) {
         // stage the keys, extend the run of rank K if it continues, then exact scores
 #pragma unroll
         for (int s = 0; s < RSLOT; ++s) {
           const int k = s * G + g;
-          if (staged && k < KT + 2) myrank[k].x = (uint32_t)rk[s];
+          if (staged && k <= KT) myrank[k].x = (uint32_t)rk[s];
         }
-        // rank K+1 is still at the head of its list; keep extracting while
-        // the keys share the top 24 bits of rank K
-        bool ext = staged && !dry && (mK1 >> 8) == tauhi;
+        // the keys past rank K are taken from lists rebuilt below mK, while
+        // they share the top 24 bits of rank K
+        bool ext = staged && rowflag == 1;
         bool bad = false;           // row-uniform: extraction can no longer be trusted
         if (__any(ext)) {
-          pop(mK1);
-          for (int k = KT + 2; k < kRmax; ++k) {
+          rebuild(zf, mK, L);
+          for (int k = KT + 1; k < kRmax; ++k) {
             if (!__any(ext)) break;
             // a lane whose list ran dry may hold the next key
             const bool dry_now = group_max_i32<G>((int)(L[0] == kKeyNone)) != 0;
