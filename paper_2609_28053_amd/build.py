@@ -11,7 +11,14 @@ import sys
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
-SOURCES = [os.path.join(CSRC, f) for f in ("eqb_api.hip", "route.hip", "margin.hip", "select.hip", "balance.hip", "variants.hip")]
+SOURCES = [os.path.join(CSRC, f) for f in ("eqb_api.hip", "margin.hip", "select.hip", "balance.hip", "variants.hip")]
+# The routing kernels are compiled on their own, without IEEE mode: their
+# float maxima and medians then need no NaN quieting, which lets the compiler
+# fold each DPP group maximum into one instruction and schedule around its
+# wait states.  Their operands are keys and finite scores, never NaN (finite
+# inputs are a precondition of the library).
+ROUTE_SOURCE = os.path.join(CSRC, "route.hip")
+ROUTE_FLAGS = ["-mno-amdgpu-ieee", "-fno-honor-nans"]
 OUT = os.path.join(HERE, "libeqb.so")
 ARCH = os.environ.get("EQB_OFFLOAD_ARCH", "gfx950")
 
@@ -28,10 +35,7 @@ FLAGS = [
 ]
 
 
-def build(verbose: bool = False, extra=()) -> str:
-    hipcc = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
-    tmp = OUT + ".tmp"
-    cmd = [hipcc, *FLAGS, *extra, "-I", os.path.join(ROOT, "include"), "-I", CSRC, *SOURCES, "-o", tmp]
+def _run(cmd, verbose):
     if verbose:
         print(" ".join(cmd), flush=True)
     res = subprocess.run(cmd, capture_output=True, text=True)
@@ -40,6 +44,20 @@ def build(verbose: bool = False, extra=()) -> str:
         raise RuntimeError(f"hipcc failed with status {res.returncode}")
     if verbose and res.stderr:
         sys.stderr.write(res.stderr)
+
+
+def build(verbose: bool = False, extra=()) -> str:
+    hipcc = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
+    tmp = OUT + ".tmp"
+    route_obj = OUT + ".route.o"
+    inc = ["-I", os.path.join(ROOT, "include"), "-I", CSRC]
+    compile_flags = [f for f in FLAGS if f != "-shared"]
+    try:
+        _run([hipcc, *compile_flags, *ROUTE_FLAGS, *extra, *inc, "-c", ROUTE_SOURCE, "-o", route_obj], verbose)
+        _run([hipcc, *FLAGS, *extra, *inc, *SOURCES, "-x", "none", route_obj, "-o", tmp], verbose)
+    finally:
+        if os.path.exists(route_obj):
+            os.remove(route_obj)
     os.replace(tmp, OUT)
     return OUT
 

@@ -173,28 +173,19 @@ __device__ __forceinline__ int key_med3(int a, int b, int c) {
 __device__ __forceinline__ bool key_lt(int a, int b) { return __int_as_float(a) < __int_as_float(b); }
 
 // Float maximum of the keys over aligned groups of G lanes, one DPP maximum
-// per level as in group_max_i32.  Each level starts with two wait states, so
-// the DPP read never follows a VALU write of its source register too closely.
+// per level as in group_max_i32.  Built without IEEE mode (the routing
+// kernels are), each level compiles to one v_max_f32_dpp, and the compiler
+// places the DPP wait states itself, filling them with independent work
+// where it can.
 template <int G>
 __device__ __forceinline__ int group_max_key(int x) {
-  if constexpr (G >= 2) {
-    // the first level writes a new register, so x itself needs no copy
-    int y;
-    asm volatile("s_nop 1\n\tv_max_f32_dpp %0, %1, %1 quad_perm:[1,0,3,2] row_mask:0xf bank_mask:0xf bound_ctrl:1"
-                 : "=v"(y) : "v"(x));
-    x = y;
-  }
-  if constexpr (G >= 4)
-    asm volatile("s_nop 1\n\tv_max_f32_dpp %0, %0, %0 quad_perm:[2,3,0,1] row_mask:0xf bank_mask:0xf bound_ctrl:1"
-                 : "+v"(x));
-  if constexpr (G >= 8)
-    asm volatile("s_nop 1\n\tv_max_f32_dpp %0, %0, %0 row_half_mirror row_mask:0xf bank_mask:0xf bound_ctrl:1"
-                 : "+v"(x));
-  if constexpr (G >= 16)
-    asm volatile("s_nop 1\n\tv_max_f32_dpp %0, %0, %0 row_mirror row_mask:0xf bank_mask:0xf bound_ctrl:1"
-                 : "+v"(x));
+  float f = __int_as_float(x);
+  if constexpr (G >= 2) f = fmaxf(f, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(f), 0xB1, 0xF, 0xF, false)));
+  if constexpr (G >= 4) f = fmaxf(f, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(f), 0x4E, 0xF, 0xF, false)));
+  if constexpr (G >= 8) f = fmaxf(f, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(f), 0x141, 0xF, 0xF, false)));
+  if constexpr (G >= 16) f = fmaxf(f, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(f), 0x140, 0xF, 0xF, false)));
   static_assert(G <= 16, "group reductions cover at most 16 lanes");
-  return x;
+  return __float_as_int(f);
 }
 
 // Value of lane S of every aligned group of G lanes (G = 1, 2, 4 or 8), by

@@ -39,23 +39,24 @@ constexpr int kRouteWaves = kRouteBlock / 64;
 template <int E> struct FastCfg { static constexpr int G = E >= 64 ? 8 : E / 8; };
 
 // The BF16 logit z of an extracted key.  The key holds the top 24 bits H of
-// s = fl32(z + b) (low byte = expert index).  When |z| >= |s| / 64, two
-// adjacent BF16 values give scores more than 256 binary32 ulps of s apart,
-// so at most one BF16 value maps to H; it is bf16(s_mid - b) with s_mid the
-// middle of the 256-ulp interval, and it is accepted only after
-// fl32(z + b) is checked to reproduce H.  The two zeros are the exception:
-// +0 and -0 give the same sum, and which one z is decides the sign of a zero
-// tau, so a zero is never accepted.  *ok reports the check; otherwise z must
-// be read from memory.
+// s = fl32(z + b) (low byte = expert index).  The candidate is
+// zc = bf16(s_mid - b), with s_mid the middle of the 256-ulp interval of H;
+// it is accepted when fl32(zc + b) reproduces H and |zc| * 64 >= |s_mid|.
+// The second test gives exponent(zc) >= exponent(s) - 6, so the BF16
+// neighbours of zc lie at least half a BF16 ulp of zc = 2^(exponent(s)-141)
+// away, about 512 binary32 ulps of s: no other BF16 value maps to H, and zc
+// is z.  s_mid is never zero, so the test also rejects both zeros (+0 and -0
+// give the same sum, and which one z is decides the sign of a zero tau), and
+// an infinite or NaN zc cannot reproduce the finite H.  *ok reports the
+// tests; otherwise z must be read from memory.
 __device__ __forceinline__ uint32_t z_from_key(int key, float b, bool* ok) {
   const uint32_t kb = (uint32_t)key;
   const float s_mid = __uint_as_float((kb & 0xFFFFFF00u) | 0x80u);
-  const uint32_t zc = bf16x2_bits(s_mid - b, 0.0f) & 0xFFFFu;
-  const uint32_t sc = __float_as_uint(__uint_as_float(zc << 16) + b);
-  const int ez = (int)((zc >> 7) & 0xFFu), es = (int)((kb >> 23) & 0xFFu);
-  // bitwise, not short-circuit: the four tests are cheap and a branch per
-  // test would cost more than they do
-  *ok = ((sc ^ kb) < 256u) & (ez >= es - 6) & ((zc & 0x7F80u) != 0x7F80u) & ((zc & 0x7FFFu) != 0u);
+  const uint32_t zc = bf16x2_bits(s_mid - b, 0.0f);   // bits 16..31: bf16(+0) = 0
+  const float zf = __uint_as_float(zc << 16);
+  const uint32_t sc = __float_as_uint(zf + b);
+  // bitwise, not short-circuit: a branch per test would cost more than it does
+  *ok = ((sc ^ kb) < 256u) & (fabsf(zf) * 64.0f >= fabsf(s_mid));
   return zc;
 }
 
@@ -216,6 +217,7 @@ __global__ __launch_bounds__(kRouteBlock) void route_fast_kernel(
   // widened, refill(raw) issues the next step's loads into the same registers.
   auto process = [&](uint2 (&raw)[NQ], uint32_t t, bool valid, auto&& refill) __attribute__((always_inline)) {
     // ---- widen the logits once; build keys and the per-lane sorted list
+    float4 bq = bias4(0);   // read first: its LDS latency passes during the widening
     float zf[N];
 #pragma unroll
     for (int q = 0; q < NQ; ++q) {
@@ -230,10 +232,15 @@ __global__ __launch_bounds__(kRouteBlock) void route_fast_kernel(
     for (int j = 0; j < kList; ++j) L[j] = kKeyNone;
 #pragma unroll
     for (int q = 0; q < NQ; ++q) {
-      const float4 bq = bias4(q);
+      // The next piece's bias is read while this piece is inserted; the
+      // scheduling barrier keeps the compiler from sinking the read to its use.
+      float4 bn = bq;
+      if (q + 1 < NQ) bn = bias4(q + 1);
+      __builtin_amdgcn_sched_barrier(0);
       const uint32_t ipk = idxpk(q);
 #pragma unroll
       for (int i = 0; i < 4; ++i) list_insert(L, key_of(zf[q * 4 + i], pick(bq, i), ipk, i));
+      bq = bn;
     }
 
     // ---- extraction rounds: group maximum of the list heads, winner pops
