@@ -360,6 +360,16 @@ __device__ __forceinline__ uint32_t hist_row(int e) { return (uint32_t)(e >> 1) 
 __device__ __forceinline__ uint32_t hist_inc(int e) { return 1u << ((e & 1) * 16); }
 
 // Rows handled by block blockIdx.x.
+// A 64-bit value every lane of the wave holds, moved to scalar registers.
+// Offsets of segment bases pass through it, so that the compiler knows the
+// bases are wave-uniform: loads and stores then take a 64-bit scalar base
+// next to a 32-bit vector offset instead of a 64-bit address per lane.
+__device__ __forceinline__ int64_t wave_uniform(int64_t x) {
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)(uint64_t)x);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)((uint64_t)x >> 32));
+  return (int64_t)(((uint64_t)hi << 32) | lo);
+}
+
 __device__ __forceinline__ void block_rows(int64_t T, int64_t rows_per_block, int64_t* r0, int64_t* r1) {
   *r0 = (int64_t)blockIdx.x * rows_per_block;
   *r1 = (*r0 + rows_per_block < T) ? *r0 + rows_per_block : T;

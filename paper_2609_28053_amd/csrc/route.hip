@@ -543,10 +543,11 @@ __global__ __launch_bounds__(kRouteBlock) void route_fast_kernel(
     uint2 buf[NQ];
     // a row past the segment reads the segment's last row; it is processed
     // as invalid (no output, no count)
-    seg_z = z + s0 * E;
-    seg_idx = topk_idx + s0 * K;
-    seg_score = topk_score + s0 * K;
-    seg_tau = tau + s0;
+    const int64_t su = wave_uniform(s0);
+    seg_z = z + su * E;
+    seg_idx = topk_idx + su * K;
+    seg_score = topk_score + su * K;
+    seg_tau = tau + su;
     const uint32_t n = (uint32_t)(s1 - s0);
     auto load_rows = [&](uint2* dst, uint32_t base) {
       uint32_t t = base + wave * R + r;
@@ -560,13 +561,13 @@ __global__ __launch_bounds__(kRouteBlock) void route_fast_kernel(
     // The next step's loads are in flight while a step is processed: a step
     // widens the rows loaded one step earlier and then reuses their registers
     // for the next step's loads, so the only wait is for loads issued a whole
-    // step before.
+    // step before.  The last step also loads (the segment's last row, clamped
+    // in load_rows), which keeps the loads unconditional: the registers then
+    // carry over to the next step without copies.
     load_rows(buf, 0);
     for (uint32_t base = 0; base < n; base += ROWS) {
       const uint32_t t = base + wave * R + r;
-      process(buf, t, t < n, [&](uint2 (&dst)[NQ]) {
-        if (base + ROWS < n) load_rows(dst, base + ROWS);
-      });
+      process(buf, t, t < n, [&](uint2 (&dst)[NQ]) { load_rows(dst, base + ROWS); });
     }
     __syncthreads();
     if (hist) {
