@@ -305,15 +305,25 @@ __global__ __launch_bounds__(kRouteBlock) void route_fast_kernel(
         bad = bad | !ok[s];
       }
       if (__builtin_expect(__any(bad), 0)) {
-        // the loads and their use stay inside a branch the whole wave takes
-        // or skips, so the common case carries no pending load
+        // The few failed recoveries are read one lane at a time with scalar
+        // loads: their wait does not include the vector loads of the next
+        // step, which are still in flight (vector loads complete in order, so
+        // a vector fallback load would wait for all of them).
 #pragma unroll
         for (int s = 0; s < RSLOT; ++s) {
+          const uint32_t off = (t * (uint32_t)E + (uint32_t)es[s]) * 2u;   // < 2^25
           uint32_t zl = zown[s];
-          if (!ok[s]) zl = at<uint16_t>(seg_z, (t * E + es[s]) * 2u);
-          zown[s] = zl | 0u;
+          uint64_t need = __ballot(!ok[s]);
+          while (need) {
+            const int l = __builtin_ctzll(need);
+            const uint32_t o = __builtin_amdgcn_readlane(off, l);
+            // the aligned word holding z (seg_z is 16-byte aligned)
+            const uint32_t w = at<const uint32_t>(seg_z, o & ~3u);
+            if (lane == l) zl = (w >> ((o & 2u) * 8u)) & 0xFFFFu;
+            need &= need - 1;
+          }
+          zown[s] = zl;
         }
-        __builtin_amdgcn_s_waitcnt(0);
       }
       const int tauhi = mK >> 8;
       const bool dry = rowflag == 2;
