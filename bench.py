@@ -194,21 +194,30 @@ def signs_leg(torch, zt, lay, run_step, reps=10, shift=4.0):
     makes every cutoff negative: a sigmoid router's logits sit mostly below
     zero, and the path should not depend on the sign of tau.  The shifted copy
     is made on the device by torch (input preparation, finished before the
-    timed steps); stage times come from events as in the main measurement."""
+    timed steps).  Shifted and unshifted steps alternate, so both see the
+    same clock and thermal state; stage times come from events as in the
+    main measurement."""
     zs = (zt.view(torch.bfloat16).float() - shift).to(torch.bfloat16).view(torch.int16)
     torch.cuda.synchronize()
     for _ in range(3):
         run_step(None, zs)
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(6)] for _ in range(reps)]
+        run_step(None, zt)
+    evs = {name: [[torch.cuda.Event(enable_timing=True) for _ in range(6)] for _ in range(reps)]
+           for name in ("shifted", "unshifted")}
     for i in range(reps):
-        run_step(evs[i], zs)
+        run_step(evs["shifted"][i], zs)
+        run_step(evs["unshifted"][i], zt)
+    torch.cuda.synchronize()
+    run_step(None, zs)
     torch.cuda.synchronize()
     frac = float((lay.tau <= 0).float().mean().item())
     del zs
-    return {"shift": -shift, "tau_nonpositive_frac": frac,
-            "route_hist1_ms": float(np.mean([e[1].elapsed_time(e[2]) for e in evs])),
-            "margin_hist2_ms": float(np.mean([e[3].elapsed_time(e[4]) for e in evs])),
-            "step_ms_median": float(np.median([e[0].elapsed_time(e[5]) for e in evs]))}
+    out = {"shift": -shift, "tau_nonpositive_frac": frac}
+    for name, e in evs.items():
+        out[name] = {"route_hist1_ms": float(np.mean([x[1].elapsed_time(x[2]) for x in e])),
+                     "margin_hist2_ms": float(np.mean([x[3].elapsed_time(x[4]) for x in e])),
+                     "step_ms_median": float(np.median([x[0].elapsed_time(x[5]) for x in e]))}
+    return out
 
 
 def per_rank_leg(eqb, torch, stream, steps=200):
