@@ -65,13 +65,17 @@ int max_blocks_cap();
 
 // Blocks and rows per block for a streaming kernel over T rows that advances
 // rows_per_step rows per block step: at most blocks_per_cu blocks per CU,
-// each owning a contiguous range of whole steps.
-inline void grid_for(int64_t T, int rows_per_step, int blocks_per_cu, int* blocks, int64_t* rows_per_block) {
+// each owning a contiguous range of whole steps, and at least min_steps
+// steps per block where T allows (a block's fixed costs, zeroing and
+// flushing its LDS counts, then pay for more rows).
+inline void grid_for(int64_t T, int rows_per_step, int blocks_per_cu, int* blocks, int64_t* rows_per_block,
+                     int min_steps = 1) {
   int64_t max_blocks = (int64_t)num_cus() * blocks_per_cu;
   const int cap = max_blocks_cap();
   if (cap > 0 && cap < max_blocks) max_blocks = cap;
   const int64_t steps = (T + rows_per_step - 1) / rows_per_step;
-  int64_t nb = steps < max_blocks ? steps : max_blocks;
+  const int64_t want = (steps + min_steps - 1) / min_steps;
+  int64_t nb = want < max_blocks ? want : max_blocks;
   if (nb < 1) nb = 1;
   const int64_t steps_per_block = (steps + nb - 1) / nb;
   *rows_per_block = steps_per_block * rows_per_step;

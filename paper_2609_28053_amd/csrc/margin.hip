@@ -127,7 +127,11 @@ eqb_status launch_margin_e(bool fine, const MarginArgs& a, hipStream_t s) {
   int blocks;
   int64_t rpb;
   const int rows_per_step = kWaves * (64 / (E / 8)) * kMarginU;
-  grid_for(a.T, rows_per_step, hist_words<E>() * 4 * 2 <= 160 * 1024 ? 2 : 1, &blocks, &rpb);
+  // At least 1,024 rows per block: at one rank's share of the paper's batch
+  // (147,456 tokens, E = 256) that roughly halves the blocks whose LDS
+  // counts are zeroed and flushed; large batches still fill every CU.
+  grid_for(a.T, rows_per_step, hist_words<E>() * 4 * 2 <= 160 * 1024 ? 2 : 1, &blocks, &rpb,
+           (1024 + rows_per_step - 1) / rows_per_step);
   if (fine)
     margin_hist_kernel<E, true><<<blocks, kBlock, 0, s>>>(a.z, a.tau, a.T, a.sel_hi, a.sel_stride, a.hist,
                                                          a.pt, rpb);
