@@ -52,6 +52,7 @@ __global__ __launch_bounds__(kBlock) void margin_hist_kernel(
   constexpr int R = 64 / G;
   constexpr int ROWS = kWaves * R * kMarginU;
   __shared__ uint32_t sh_hist[hist_words<E>()];
+  __shared__ int32_t sh_sel[kFine ? E : 1];   // the segment's selections, for the flush
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int g = lane % G, rr = lane / G;
@@ -67,6 +68,11 @@ __global__ __launch_bounds__(kBlock) void margin_hist_kernel(
   // be held by the memory-side cache.
   for_each_segment_rev(r0, r1, pt, [&](int p, int64_t s0, int64_t s1) {
     const int32_t* sel = kFine ? sel_hi + (int64_t)p * sel_stride : nullptr;
+    if (kFine) {
+      // read once here: the flush looks a selection up per populated bin,
+      // and a global load there would sit on its critical path
+      for (int e = threadIdx.x; e < E; e += kBlock) sh_sel[e] = sel[e];
+    }
     uint32_t csel[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
@@ -116,7 +122,7 @@ __global__ __launch_bounds__(kBlock) void margin_hist_kernel(
     if (!kFine) {
       flush_hist<E, false>(sh_hist, slab, nullptr);
     } else {
-      flush_hist<E, true>(sh_hist, slab, sel);
+      flush_hist<E, true>(sh_hist, slab, sh_sel);
     }
     __syncthreads();
   });
