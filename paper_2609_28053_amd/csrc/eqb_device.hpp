@@ -159,6 +159,7 @@ __device__ __forceinline__ int med3_i32(int a, int b, int c) {
 // per-lane functions of their operands, so the asm is not volatile and the
 // compiler may schedule loads across it.
 constexpr int kKeyNone = (int)0xFF800000u;   // -inf: below every key
+constexpr int kKeyTop = (int)0x7F800000u;    // +inf: above every key
 
 __device__ __forceinline__ int key_max(int a, int b) {
   int r;

@@ -361,7 +361,38 @@ __global__ __launch_bounds__(kRouteBlock) void route_fast_kernel(
           }
         }
         bad = bad || ext;           // the run is longer than the rank buffer
-        slow = slow || bad || (staged && dry);
+        // Rows where a lane's list ran dry redo the extraction from fresh
+        // lists, refilling a lane's list below its last key whenever it runs
+        // dry again (as the generic-K loop does); only a run longer than the
+        // rank buffer still goes to the exact 64-bit path.
+        bool redo = staged && dry;
+        if (__any(redo)) {
+          if (redo) rebuild(zf, kKeyTop, L);
+          bool done = !redo;
+          int th = 0;
+#pragma unroll 1
+          for (int k = 0; k < kRmax; ++k) {
+            if (!__any(!done)) break;
+            const int M = group_max_key<G>(L[0]);
+            pop(M);
+            const bool dl = (L[0] == kKeyNone) && (M != kKeyNone);
+            if (__any(dl && !done)) {
+              if (dl && !done) rebuild(zf, M, L);
+            }
+            if (!done) {
+              if (M == kKeyNone) {
+                done = true;
+              } else {
+                if (g == 0) myrank[k].x = (uint32_t)M;
+                nrank = k + 1;
+                if (k == K) th = M >> 8;
+                if (k > K && (M >> 8) != th) done = true;   // one key past the run of rank K
+              }
+            }
+          }
+          bad = bad || !done;
+        }
+        slow = slow || bad;
         staged = staged && !slow;
         lds_wave_sync();
 #pragma unroll

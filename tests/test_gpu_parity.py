@@ -128,6 +128,31 @@ def test_every_E_and_K_extremes(eqb, E):
             assert_parity(gpu_layer(eqb, z, b, K, off), O.run_layer(z, b, K, off), K)
 
 
+@pytest.mark.parametrize("E,K", [(64, 8), (64, 6), (128, 6), (256, 8), (256, 6)])
+def test_lists_run_dry(eqb, E, K):
+    """Rows whose top ranks crowd into the experts of one lane.  The fast
+    route kernel keeps six keys per lane (lane g of a row holds the experts
+    with (e >> 2) % 8 == g); a lane holding more of the top K+1 keys runs
+    dry, and the row is extracted again with refilled lists.  Some rows also
+    carry exact ties, so dry rows meet the exact ordering of tied scores."""
+    rng = np.random.default_rng(1000 + E + K)
+    T = 3001
+    x = rng.standard_normal((T, E)).astype(np.float32)
+    lane = (np.arange(E) >> 2) % 8
+    hot = rng.integers(0, 8, T)
+    crowd = rng.random(T) < 0.6
+    boost = np.where(crowd[:, None] & (lane[None, :] == hot[:, None]), np.float32(6.0), np.float32(0.0))
+    x = x + boost
+    tie_rows = rng.random(T) < 0.2
+    x[tie_rows] = np.round(x[tie_rows] * 2) / 2          # many equal logits in these rows
+    z = O.f32_to_bf16_rne(x.astype(np.float32))
+    b = np.zeros(E, np.float32)
+    b[rng.integers(0, E, 5)] = np.float32(0.25)
+    off = np.array([0, 1000, 2001, T], np.int64)
+    say(f"dry lists E={E} K={K} T={T}")
+    assert_parity(gpu_layer(eqb, z, b, K, off), O.run_layer(z, b, K, off), K)
+
+
 @pytest.mark.parametrize("zbits", [0x3F00, 0xBF00, 0x8000], ids=["half", "minus_half", "minus_zero"])
 @pytest.mark.parametrize("bzero", [0.0, -0.0], ids=["b_plus0", "b_minus0"])
 def test_all_ties_constant_logits(eqb, zbits, bzero):
