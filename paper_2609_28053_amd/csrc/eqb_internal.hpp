@@ -65,9 +65,13 @@ int max_blocks_cap();
 
 // Blocks and rows per block for a streaming kernel over T rows that advances
 // rows_per_step rows per block step: at most blocks_per_cu blocks per CU,
-// each owning a contiguous range of whole steps, and at least min_steps
-// steps per block where T allows (a block's fixed costs, zeroing and
-// flushing its LDS counts, then pay for more rows).
+// each owning a contiguous range of ceil(T / blocks) rows (the last may be
+// shorter), and at least min_steps steps per block where T allows (a
+// block's fixed costs, zeroing and flushing its LDS counts, then pay for
+// more rows).  The ranges are not rounded to whole steps: with P equal
+// partitions and a block count that P divides, every partition boundary
+// then falls on a block boundary, and no block pays for a second segment
+// (a second flush and a cold restart of its prefetch).
 inline void grid_for(int64_t T, int rows_per_step, int blocks_per_cu, int* blocks, int64_t* rows_per_block,
                      int min_steps = 1) {
   int64_t max_blocks = (int64_t)num_cus() * blocks_per_cu;
@@ -77,9 +81,9 @@ inline void grid_for(int64_t T, int rows_per_step, int blocks_per_cu, int* block
   const int64_t want = (steps + min_steps - 1) / min_steps;
   int64_t nb = want < max_blocks ? want : max_blocks;
   if (nb < 1) nb = 1;
-  const int64_t steps_per_block = (steps + nb - 1) / nb;
-  *rows_per_block = steps_per_block * rows_per_step;
+  *rows_per_block = T > 0 ? (T + nb - 1) / nb : 1;
   *blocks = (int)((T + *rows_per_block - 1) / *rows_per_block);
+  if (*blocks < 1) *blocks = 1;
 }
 
 inline eqb_status launch_status() { return hipGetLastError() == hipSuccess ? EQB_OK : EQB_ERR_HIP; }
