@@ -382,3 +382,50 @@ def test_token_permutation_on_gpu(eqb):
     for k in ("load", "H", "L", "u", "v", "rho", "bhat"):
         np.testing.assert_array_equal(c[k], a[k])
     np.testing.assert_array_equal(c["b_next"].view(np.uint32), a["b_next"].view(np.uint32))
+
+
+def test_expert_permutation_on_gpu(eqb):
+    """Permuting the experts (columns of z together with b) permutes every
+    per-expert statistic; the cutoffs do not move (tau is a value of the row)."""
+    w, z, b, off = workload("large256", 30011, 4)
+    perm = np.random.default_rng(11).permutation(w.E)
+    say("expert permutation")
+    a = gpu_layer(eqb, z, b, w.K, off)
+    c = gpu_layer(eqb, np.ascontiguousarray(z[:, perm]), np.ascontiguousarray(b[perm]), w.K, off)
+    np.testing.assert_array_equal(c["tau"].view(np.uint32), a["tau"].view(np.uint32))
+    np.testing.assert_array_equal(c["H_p"], a["H_p"][:, perm])
+    np.testing.assert_array_equal(c["L_p"], a["L_p"][:, perm])
+    for k in ("u", "rho", "v", "bhat"):
+        np.testing.assert_array_equal(c[k], a[k][perm])
+    np.testing.assert_array_equal(c["b_next"].view(np.uint32), a["b_next"][perm].view(np.uint32))
+    # the selected experts are the same set (and loads follow them) wherever
+    # the row has no tie at the cutoff, which the index rule would break
+    # differently after the permutation
+    zf = (z.astype(np.uint32) << 16).view(np.float32)
+    s = zf + b[None, :]
+    tau = a["tau"]
+    untied = (s == tau[:, None]).sum(1) == 1
+    sel_a = np.sort(a["idx"][untied], axis=1)
+    sel_c = np.sort(perm[c["idx"][untied]], axis=1)
+    np.testing.assert_array_equal(sel_c, sel_a)
+    assert untied.mean() > 0.9
+
+
+def test_common_bias_shift_on_gpu(eqb):
+    """With logits and bias on the quarter-step grid every sum and every
+    margin is exact (margins stay within BF16's 8 significant bits): adding
+    1/4 to every bias leaves the routing unchanged, moves tau and the
+    quantile by exactly 1/4, and leaves the centred bias unchanged (Eq. 2:
+    only differences of b matter)."""
+    w, z, _, off = workload("tie64", 50021, 2)
+    b = (np.random.default_rng(5).integers(-4, 5, size=w.E) / 4).astype(np.float32)
+    say("common bias shift")
+    a = gpu_layer(eqb, z, b, w.K, off)
+    c = gpu_layer(eqb, z, (b + np.float32(0.25)).astype(np.float32), w.K, off)
+    np.testing.assert_array_equal(c["idx"], a["idx"])
+    np.testing.assert_array_equal(c["load"], a["load"])
+    np.testing.assert_array_equal(c["tau"], a["tau"] + np.float32(0.25))
+    qa = (a["bhat"].astype(np.uint32) << 16).view(np.float32)
+    qc = (c["bhat"].astype(np.uint32) << 16).view(np.float32)
+    np.testing.assert_array_equal(qc, qa + np.float32(0.25))
+    np.testing.assert_array_equal(c["b_next"], a["b_next"])
