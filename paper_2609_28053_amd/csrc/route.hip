@@ -37,6 +37,7 @@ constexpr int kRouteBlock = 768;
 constexpr int kRouteWaves = kRouteBlock / 64;
 
 template <int E> struct FastCfg { static constexpr int G = E >= 64 ? 8 : E / 8; };
+constexpr int kBiasPad = 32;           // words between the rotated bias copies beyond E
 
 // The BF16 logit z of an extracted key.  The key holds the top 24 bits H of
 // s = fl32(z + b) (low byte = expert index).  The candidate is
@@ -142,7 +143,11 @@ __global__ __launch_bounds__(kRouteBlock) void route_fast_kernel(
   __shared__ uint32_t sh_hist[fast_hist_words<E>()];
   __shared__ uint32_t sh_load[E];
   __shared__ float sh_b[E];             // b as given: exact scores and tau
-  __shared__ float sh_bk[NQ][E];        // b with -0 as +0 (the keys' sums), per piece rotation
+  // b with -0 as +0 (the keys' sums), one copy per piece rotation.  Copies
+  // sit E + 32 words apart: the rows of a wave read their rotations' copies
+  // with one 16-byte read per lane, and copies E words apart (a multiple of
+  // the 64 banks) would put every row's reads on the same 32 banks.
+  __shared__ float sh_bk[NQ][E + kBiasPad];
   __shared__ uint2 sh_rank[kRouteWaves][R][kRmax];   // (score bits, zbits << 16 | e) in rank order
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
