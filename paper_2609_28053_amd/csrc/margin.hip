@@ -13,6 +13,7 @@
 namespace eqb {
 
 constexpr int kMarginU = 4;   // rows per lane per block step
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
 // Counts the margins of one row piece: eight experts e0 .. e0+7 (four packed
 // BF16 pairs in w) against tau.  Two margins are rounded by one conversion;
@@ -100,7 +101,11 @@ __global__ __launch_bounds__(kBlock) void margin_hist_kernel(
       for (int u = 0; u < kMarginU; ++u) {
         uint32_t t = base + (uint32_t)((u * kWaves + wave) * R + rr);
         t = t < n ? t : n - 1;
-        v[u] = *reinterpret_cast<const uint4*>(seg_z + (t * (uint32_t)E + (uint32_t)e0) * 2u);
+        // z is read once per sweep and not again in this layer: a
+        // non-temporal load streams it without allocating it in the caches
+        const u32x4 x = __builtin_nontemporal_load(
+            reinterpret_cast<const u32x4*>(seg_z + (t * (uint32_t)E + (uint32_t)e0) * 2u));
+        v[u] = make_uint4(x.x, x.y, x.z, x.w);
         tv[u] = *reinterpret_cast<const float*>(seg_tau + t * 4u);
       }
     };
