@@ -168,6 +168,33 @@ __global__ __launch_bounds__(kRouteBlock) void route_fast_kernel(
   auto bias4x = [&](int q) -> float4 { return *reinterpret_cast<const float4*>(&sh_b[ex(q)]); };
   auto pick = [](const float4& v, int i) -> float { return i == 0 ? v.x : i == 1 ? v.y : i == 2 ? v.z : v.w; };
 
+  // Rows of one step of a segment starting at zb and holding n rows: row
+  // base + wave * R + r of the segment, a row past its end reading the last
+  // row instead (processed as invalid: no output, no count).  Byte offsets
+  // stay below 2^25; the piece index occupies bits that the row and lane
+  // parts leave clear, so XOR selects piece q ^ rr.
+  auto load_step = [&](uint2 (&dst)[NQ], const uint16_t* zb, uint32_t base, uint32_t n) {
+    uint32_t t = base + wave * R + r;
+    t = t < n ? t : n - 1;
+    const uint32_t off = (t * (uint32_t)E + (uint32_t)g * 4u) * 2u + (uint32_t)rr * (8u * G);
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) dst[q] = at<uint2>(zb, off ^ ((uint32_t)q * (8u * G)));
+  };
+
+  // The first step of the block's first segment (as for_each_segment will
+  // cut it) is loaded before the LDS set-up, so that its latency passes while
+  // the histogram is zeroed and the bias is staged.
+  int64_t r0, r1;
+  block_rows(T, rows_per_block, &r0, &r1);
+  uint2 buf[NQ];
+  if (r0 < r1) {
+    int p = 0;
+    while (p < pt.P - 1 && pt.off[p + 1] <= r0) ++p;
+    int64_t end = pt.off[p + 1] < r1 ? pt.off[p + 1] : r1;
+    if (end - r0 > kSegMax) end = r0 + kSegMax;
+    load_step(buf, z + wave_uniform(r0) * E, 0, (uint32_t)(end - r0));
+  }
+
   for (int w = threadIdx.x; w < fast_hist_words<E>(); w += kRouteBlock) sh_hist[w] = 0;
   int fits = 1;
   for (int e = threadIdx.x; e < E; e += kRouteBlock) {
@@ -183,8 +210,6 @@ __global__ __launch_bounds__(kRouteBlock) void route_fast_kernel(
   // z + b is finite and every key is a finite float.
   const bool bias_ok = __syncthreads_and(fits) != 0;
 
-  int64_t r0, r1;
-  block_rows(T, rows_per_block, &r0, &r1);
   uint2* myrank = sh_rank[wave][r];
 
   // key of element (q, i) from its widened logit
@@ -585,35 +610,26 @@ __global__ __launch_bounds__(kRouteBlock) void route_fast_kernel(
     __builtin_amdgcn_wave_barrier();
   };
 
+  bool first = true;
   for_each_segment(r0, r1, pt, [&](int p, int64_t s0, int64_t s1) {
-    uint2 buf[NQ];
-    // a row past the segment reads the segment's last row; it is processed
-    // as invalid (no output, no count)
     const int64_t su = wave_uniform(s0);
     seg_z = z + su * E;
     seg_idx = topk_idx + su * K;
     seg_score = topk_score + su * K;
     seg_tau = tau + su;
     const uint32_t n = (uint32_t)(s1 - s0);
-    auto load_rows = [&](uint2* dst, uint32_t base) {
-      uint32_t t = base + wave * R + r;
-      t = t < n ? t : n - 1;
-      // bytes, < 2^25; the piece index occupies bits that the row and lane
-      // parts leave clear, so XOR selects piece q ^ rr
-      const uint32_t off = (t * (uint32_t)E + (uint32_t)g * 4u) * 2u + (uint32_t)rr * (8u * G);
-#pragma unroll
-      for (int q = 0; q < NQ; ++q) dst[q] = at<uint2>(seg_z, off ^ ((uint32_t)q * (8u * G)));
-    };
     // The next step's loads are in flight while a step is processed: a step
     // widens the rows loaded one step earlier and then reuses their registers
     // for the next step's loads, so the only wait is for loads issued a whole
     // step before.  The last step also loads (the segment's last row, clamped
-    // in load_rows), which keeps the loads unconditional: the registers then
-    // carry over to the next step without copies.
-    load_rows(buf, 0);
+    // in load_step), which keeps the loads unconditional: the registers then
+    // carry over to the next step without copies.  The first segment's first
+    // step was loaded before the LDS set-up.
+    if (!first) load_step(buf, seg_z, 0, n);
+    first = false;
     for (uint32_t base = 0; base < n; base += ROWS) {
       const uint32_t t = base + wave * R + r;
-      process(buf, t, t < n, [&](uint2 (&dst)[NQ]) { load_rows(dst, base + ROWS); });
+      process(buf, t, t < n, [&](uint2 (&dst)[NQ]) { load_step(dst, seg_z, base + ROWS, n); });
     }
     __syncthreads();
     if (hist) {

@@ -64,6 +64,9 @@ __global__ __launch_bounds__(kNBins) void select_fine_kernel(
     }
     return;
   }
+  // the coarse choice is read first: its load overlaps those of the counts
+  const int u = sel_hi[out];
+  const int64_t rho = rank_in_bin[out];
   int64_t c = 0;
   if (kLocal) {
     c = hist[((int64_t)p * E + e) * kNBins + v];
@@ -72,8 +75,6 @@ __global__ __launch_bounds__(kNBins) void select_fine_kernel(
     if (hist_sum) hist_sum[(int64_t)e * kNBins + v] = (int32_t)c;
   }
   const int64_t cum = block_inclusive_scan_256(c, sh);
-  const int u = sel_hi[out];
-  const int64_t rho = rank_in_bin[out];
   const bool ok = u >= 0 && u < kNBins && rho >= 1;
   if (ok && cum >= rho && cum - c < rho) {
     sel_lo[out] = v;
