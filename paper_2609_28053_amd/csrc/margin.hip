@@ -12,7 +12,7 @@
 
 namespace eqb {
 
-constexpr int kMarginU = 4;   // rows per lane per block step
+constexpr int kMarginU = 3;   // rows per lane per block step
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
 // Counts the margins of one row piece: eight experts e0 .. e0+7 (four packed
@@ -52,14 +52,16 @@ __global__ __launch_bounds__(kBlock) void margin_hist_kernel(
   constexpr int G = E / 8;
   constexpr int R = 64 / G;
   constexpr int ROWS = kWaves * R * kMarginU;
-  __shared__ uint32_t sh_hist[hist_words<E>()];
+  __shared__ __align__(16) uint32_t sh_hist[hist_words<E>()];
   __shared__ int32_t sh_sel[kFine ? E : 1];   // the segment's selections, for the flush
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int g = lane % G, rr = lane / G;
   const int e0 = g * 8;
   const uint32_t row0 = hist_row(e0);
-  for (int w = threadIdx.x; w < hist_words<E>(); w += kBlock) sh_hist[w] = 0;
+  for (int w = threadIdx.x; w < hist_words<E>() / 4; w += kBlock)
+    reinterpret_cast<uint4*>(sh_hist)[w] = make_uint4(0, 0, 0, 0);
+  for (int w = (hist_words<E>() / 4) * 4 + threadIdx.x; w < hist_words<E>(); w += kBlock) sh_hist[w] = 0;
   __syncthreads();
 
   int64_t r0, r1;

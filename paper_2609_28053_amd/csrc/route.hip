@@ -140,7 +140,7 @@ __global__ __launch_bounds__(kRouteBlock) void route_fast_kernel(
   static_assert(KT == 0 || KT + 2 <= E, "K+2 keys must exist");
   const int K = KT > 0 ? KT : Kdyn;
 
-  __shared__ uint32_t sh_hist[fast_hist_words<E>()];
+  __shared__ __align__(16) uint32_t sh_hist[fast_hist_words<E>()];
   __shared__ uint32_t sh_load[E];
   __shared__ float sh_b[E];             // b as given: exact scores and tau
   // b with -0 as +0 (the keys' sums), one copy per piece rotation.  Copies
@@ -195,7 +195,9 @@ __global__ __launch_bounds__(kRouteBlock) void route_fast_kernel(
     load_step(buf, z + wave_uniform(r0) * E, 0, (uint32_t)(end - r0));
   }
 
-  for (int w = threadIdx.x; w < fast_hist_words<E>(); w += kRouteBlock) sh_hist[w] = 0;
+  static_assert(fast_hist_words<E>() % 4 == 0, "16-byte zeroing");
+  for (int w = threadIdx.x; w < fast_hist_words<E>() / 4; w += kRouteBlock)
+    reinterpret_cast<uint4*>(sh_hist)[w] = make_uint4(0, 0, 0, 0);
   int fits = 1;
   for (int e = threadIdx.x; e < E; e += kRouteBlock) {
     sh_load[e] = 0;
