@@ -168,15 +168,6 @@ def sigmoid64(x: np.ndarray) -> np.ndarray:
     return out
 
 
-def partition_of(T: int, part_off) -> np.ndarray:
-    """Partition number of every token for contiguous partitions."""
-    off = np.asarray(part_off, dtype=np.int64)
-    p = np.empty(T, np.int64)
-    for q in range(len(off) - 1):
-        p[off[q]:off[q + 1]] = q
-    return p
-
-
 def expert_load(idx: np.ndarray, E: int, part_off) -> np.ndarray:
     """f_{p,e} = #{t in partition p : e in I_t} (Sec. 2), int64 [P,E]."""
     off = np.asarray(part_off, dtype=np.int64)

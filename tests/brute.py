@@ -23,6 +23,67 @@ def bf16_value(bits: int) -> float:
     return f32((bits & 0xFFFF) << 16)
 
 
+def f32_fraction(bits: int) -> Fraction:
+    """Exact value of a finite binary32 pattern, decoded from its fields."""
+    bits &= 0xFFFFFFFF
+    sign = -1 if bits >> 31 else 1
+    ex = (bits >> 23) & 0xFF
+    man = bits & 0x7FFFFF
+    assert ex != 0xFF, "finite values only"
+    if ex == 0:                                   # subnormal: man * 2^-149
+        return sign * Fraction(man, 1 << 149)
+    val = Fraction((1 << 23) | man) * (Fraction(2) ** (ex - 150))
+    return sign * val
+
+
+def f32_rne_bits(q: Fraction, zero_sign: int = 0) -> int:
+    """binary32 pattern of the exact rational q rounded to nearest, ties to
+    even (IEEE 754 roundTiesToEven), with subnormals kept.  A zero result
+    takes the sign bit zero_sign (an exact zero sum is +0 unless both addends
+    are -0).  Written from the format's definition; no float conversion."""
+    if q == 0:
+        return (zero_sign & 1) << 31
+    sign = 1 if q < 0 else 0
+    a = -q if sign else q
+    # binade: 2^e <= a < 2^(e+1)
+    e = a.numerator.bit_length() - a.denominator.bit_length()
+    if Fraction(2) ** e > a:
+        e -= 1
+    assert Fraction(2) ** e <= a < Fraction(2) ** (e + 1)
+    ulp_exp = max(e, -126) - 23                  # spacing of binary32 values near a
+    m = a / (Fraction(2) ** ulp_exp)              # a in units of that spacing
+    n = m.numerator // m.denominator
+    rem = m - n
+    if rem > Fraction(1, 2) or (rem == Fraction(1, 2) and n % 2 == 1):
+        n += 1
+    # n * 2^ulp_exp is the rounded magnitude; re-normalise a carry to 2^24
+    if n == 1 << 24:
+        n >>= 1
+        ulp_exp += 1
+    if n >= 1 << 23:                              # normal
+        biased = ulp_exp + 23 + 127
+        assert 1 <= biased <= 254, "overflow is outside the inputs' domain"
+        return (sign << 31) | (biased << 23) | (n - (1 << 23))
+    return (sign << 31) | n                       # subnormal (ulp_exp = -149)
+
+
+def f32_add_rne_bits(x_bits: int, y_bits: int) -> int:
+    """binary32 sum x + y (round to nearest even) from the exact rational sum."""
+    both_neg_zero = (x_bits & 0xFFFFFFFF) == 0x80000000 and (y_bits & 0xFFFFFFFF) == 0x80000000
+    return f32_rne_bits(f32_fraction(x_bits) + f32_fraction(y_bits), 1 if both_neg_zero else 0)
+
+
+def biased_scores_exact(z_bits, b) -> list:
+    """s_{t,e} = z_{t,e} + b_e (Sec. 2, I_t = TopK(z_t + b)) as binary32 patterns,
+    each rounded once from the exact rational sum.  z_bits: BF16 patterns
+    [T][E], b: binary32 values [E].  Returns a list of rows of uint32 patterns."""
+    b_bits = [f32_bits(float(v)) for v in b]
+    out = []
+    for row in z_bits:
+        out.append([f32_add_rne_bits((int(zb) & 0xFFFF) << 16, b_bits[e]) for e, zb in enumerate(row)])
+    return out
+
+
 def topk_subset(s, K):
     """The valid Top-K subset preferred by the lower-index rule.
 

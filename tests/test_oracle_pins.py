@@ -149,9 +149,11 @@ def test_topk_and_tau_against_brute_force(E, grid):
     rng = np.random.default_rng(100 * E + grid)
     for trial in range(4):
         z, b = _tiny_rows(rng, 12, E, grid)
+        # s from the exact rational sums, rounded by the brute-force helper
+        s_bits = np.array(brute.biased_scores_exact(z, b), np.uint32)
+        s = s_bits.view(np.float32)
         for K in range(1, E):
             idx, score, tau = O.route_topk(z, b, K)
-            s = O.biased_scores(z, b)
             for t in range(z.shape[0]):
                 row = [float(v) for v in s[t]]
                 want = brute.topk_subset(row, K)
@@ -160,7 +162,7 @@ def test_topk_and_tau_against_brute_force(E, grid):
                 assert float(tau[t]) == float(tau_val)
                 # the bit pattern is the one of the element ranked K-th (0-based)
                 full = sorted(range(E), key=lambda e: (-row[e], e))
-                assert tau[t].view(np.uint32) == s[t, full[K]].view(np.uint32)
+                assert tau[t].view(np.uint32) == s_bits[t, full[K]]
 
 
 def test_scores_are_unbiased_sigmoid():
@@ -176,12 +178,49 @@ def test_scores_are_unbiased_sigmoid():
             assert abs(int(score[t, k].view(np.int32)) - int(ref.view(np.int32))) <= 1
 
 
+def _f32(v):
+    return np.float32(v)
+
+
+@pytest.mark.parametrize("case", ["random", "ties", "tiny", "zeros"])
+def test_biased_scores_equal_rounded_exact_sums(case):
+    """Reading R1 (Sec. 2, I_t = TopK(z_t + b)): s = z + b is one binary32
+    addition rounded to nearest, ties to even.  The reference rounds the
+    exact rational sum itself (tests/brute.py), never a float add."""
+    rng = np.random.default_rng({"random": 1, "ties": 2, "tiny": 3, "zeros": 4}[case])
+    if case == "random":
+        # logits of every scale, biases with full 24-bit significands
+        z = rng.integers(0, 65536, size=(64, 16), dtype=np.uint32).astype(np.uint16)
+        z[(z & 0x7F80) == 0x7F80] &= 0xBFFF           # keep them finite
+        b = (rng.standard_normal(16) * 2.0 ** rng.integers(-30, 30, size=16)).astype(np.float32)
+    elif case == "ties":
+        # z = 1 + k/128 and b = (2j+1) * 2^-24 put z + b exactly halfway
+        # between two binary32 neighbours: the even one must win
+        z = O.f32_to_bf16_rne((1.0 + np.arange(64) / 128.0).astype(np.float32))[:, None].repeat(8, 1)
+        b = ((2 * np.arange(8) + 1) * 2.0 ** -24).astype(np.float32)
+        b[4:] = -b[4:]
+    elif case == "tiny":
+        # subnormal and smallest-normal sums
+        z = np.array([[0x0000, 0x8000, 0x0080, 0x8080, 0x0001, 0x8001, 0x0081, 0x0100]] * 8, np.uint16)
+        b = np.array([2.0 ** -149, -(2.0 ** -149), 2.0 ** -126, -(2.0 ** -126) + 2.0 ** -149,
+                      3 * 2.0 ** -149, -(2.0 ** -127), 2.0 ** -130, -(2.0 ** -125)], np.float32)
+    else:
+        # signed zeros: -0 + -0 = -0, every other exact zero sum is +0
+        z = np.array([[0x0000, 0x8000, 0x8000, 0x3F80, 0xBF80, 0x0000]], np.uint16)
+        b = np.array([-0.0, -0.0, 0.0, -1.0, 1.0, 0.0], np.float32)
+    want = np.array(brute.biased_scores_exact(z, b), np.uint32)
+    got = O.biased_scores(z, b).view(np.uint32)
+    assert np.array_equal(got, want)
+    if case == "zeros":
+        assert [hex(x) for x in want[0]] == ["0x0", "0x80000000", "0x0", "0x0", "0x0", "0x0"]
+
+
 def test_topk_matches_stable_argsort_on_tie_free_rows():
     rng = np.random.default_rng(9)
     z = O.f32_to_bf16_rne(rng.standard_normal((500, 64)).astype(np.float32))
     b = (rng.standard_normal(64) * 0.1).astype(np.float32)
     idx, _, tau = O.route_topk(z, b, 6)
-    s = O.biased_scores(z, b)
+    s = np.array(brute.biased_scores_exact(z, b), np.uint32).view(np.float32)
     order = np.argsort(-s, axis=1, kind="stable")
     assert np.array_equal(idx, order[:, :6])
     assert np.array_equal(tau, np.sort(s, axis=1)[:, -7])
@@ -218,7 +257,7 @@ def test_quantile_rank_rule():
 def _brute_layer(z, b, K, part_off):
     """Everything from subsets, rationals, torch rounding and plain loops."""
     T, E = z.shape
-    s = O.biased_scores(z, b)
+    s = np.array(brute.biased_scores_exact(z, b), np.uint32).view(np.float32)
     zf = O.bf16_to_f32(z)
     idx = np.array([brute.topk_subset([float(v) for v in s[t]], K) for t in range(T)])
     order = [sorted(range(E), key=lambda e: (-float(s[t, e]), e)) for t in range(T)]
@@ -527,6 +566,18 @@ def _mut_round_truncate(x):
     return (np.ascontiguousarray(x, np.float32).view(np.uint32) >> 16).astype(np.uint16)
 
 
+def _mut_scores_rounded_to_bf16(z_bits, b):
+    # s kept only to BF16 precision
+    s = O.bf16_to_f32(z_bits) + np.asarray(b, np.float32)[None, :]
+    return O.bf16_to_f32(O.f32_to_bf16_rne(s))
+
+
+def _mut_bias_truncated_to_bf16(z_bits, b):
+    # the bias cut to its top 16 bits before the addition
+    bt = (np.asarray(b, np.float32).view(np.uint32) & 0xFFFF0000).view(np.float32)
+    return O.bf16_to_f32(z_bits) + bt[None, :]
+
+
 _orig_route = O.route_topk
 _PLANT_B = np.array([0.0, 0.25, -0.5, 0.125], np.float32)
 
@@ -561,3 +612,28 @@ def test_pins_catch_planted_mistakes(monkeypatch, attr, mutant):
             caught = True
             break
     assert caught, f"planted mistake in {attr} was not caught"
+
+
+@pytest.mark.parametrize("mutant", [_mut_scores_rounded_to_bf16, _mut_bias_truncated_to_bf16])
+def test_pins_catch_planted_score_mistakes(monkeypatch, mutant):
+    """A mistake in the binary32 sum z + b (reading R1) must fail the pins on
+    tie-free rows whose sums are inexact: the direct rounding pin and the
+    brute-force layer, which takes its scores from exact rational sums."""
+    monkeypatch.setattr(O, "biased_scores", mutant)
+    with pytest.raises(AssertionError):
+        test_biased_scores_equal_rounded_exact_sums("random")
+    rng = np.random.default_rng(78)
+    caught = 0
+    for trial in range(4):
+        T, E, K = 9, 5, int(rng.integers(1, 4))
+        z = O.f32_to_bf16_rne(rng.standard_normal((T, E)).astype(np.float32))
+        # full 24-bit significands: no sum is exact in BF16, and no two are equal
+        b = (rng.standard_normal(E) * 0.37).astype(np.float32)
+        s_exact = np.array(brute.biased_scores_exact(z, b), np.uint32)
+        assert len({int(x) for x in s_exact.ravel()}) == s_exact.size        # tie-free
+        assert np.all(s_exact & 0xFFFF)                                      # inexact in BF16
+        try:
+            check_layer_against_brute(z, b, K, np.array([0, 4, T], np.int64))
+        except AssertionError:
+            caught += 1
+    assert caught == 4, "a planted mistake in biased_scores was not caught by the layer pin"
