@@ -153,6 +153,59 @@ def test_lists_run_dry(eqb, E, K):
     assert_parity(gpu_layer(eqb, z, b, K, off), O.run_layer(z, b, K, off), K)
 
 
+# Every routing kernel the library dispatches for E >= 64: the unrolled K = 2
+# kernel on an ordinary bias (its common path), the generic-K fast kernel
+# (extraction loop with list refills, G = 8 lanes per row) for the K it
+# serves, and the exact 64-bit kernel above K = 14 (Sec. 2 allows any
+# 1 <= K < E).
+ROUTE_VARIANTS = [(E, K) for E in (64, 128, 256) for K in (3, 5, 7, 10, 14)] + \
+    [(64, 2), (256, 2), (256, 15), (256, 16)]
+
+
+def _variant_inputs(E, K, T):
+    """Skewed logits (per-expert offsets, an ordinary binary32 bias) with
+    three kinds of hard rows mixed in: rows whose top ranks crowd into the
+    experts of one lane of the fast kernel (lane g holds (e >> 2) % 8 == g),
+    so its list runs dry; rows on a half-step grid, full of exact ties, also
+    at the cutoff; and rows whose logits are all equal."""
+    rng = np.random.default_rng(7000 + 17 * E + K)
+    x = (rng.standard_normal((T, E)) + rng.standard_normal(E) * 0.7).astype(np.float32)
+    kind = rng.random(T)
+    lane = (np.arange(E) >> 2) % 8
+    hot = rng.integers(0, 8, T)
+    crowd = kind < 0.08
+    x = x + np.where(crowd[:, None] & (lane[None, :] == hot[:, None]), np.float32(5.0), np.float32(0.0))
+    grid = (kind >= 0.08) & (kind < 0.18)
+    x[grid] = np.round(x[grid] * 2) / 2
+    flat = kind >= 0.995
+    x[flat] = np.float32(0.5)
+    z = O.f32_to_bf16_rne(x.astype(np.float32))
+    b = (rng.standard_normal(E) * 0.1).astype(np.float32)
+    cuts = np.sort(rng.choice(np.arange(1, T), size=2, replace=False))
+    off = np.array([0, cuts[0], cuts[1], T], np.int64)
+    return z, b, off
+
+
+@pytest.mark.parametrize("E,K", ROUTE_VARIANTS, ids=[f"E{e}-K{k}" for e, k in ROUTE_VARIANTS])
+def test_route_variants(eqb, E, K):
+    """Each shipped routing kernel against the oracle at the default grid and
+    with one block, whose rows then span three 65,535-row segments (three LDS
+    flushes of one partition, one of them across a partition boundary)."""
+    T = 2 * 65535 + 31
+    z, b, off = _variant_inputs(E, K, T)
+    say(f"route variant E={E} K={K} T={T}: oracle")
+    want = O.run_layer(z, b, K, off, threads=_threads())
+    for cap in (0, 1, 5):
+        say(f"route variant E={E} K={K} T={T} grid cap {cap}")
+        try:
+            eqb.eqb_set_max_blocks(cap)
+            assert_parity(gpu_layer(eqb, z, b, K, off, fused=True), want, K)
+            if cap == 0:
+                assert_parity(gpu_layer(eqb, z, b, K, off, fused=False), want, K)
+        finally:
+            eqb.eqb_set_max_blocks(0)
+
+
 @pytest.mark.parametrize("zbits", [0x3F00, 0xBF00, 0x8000], ids=["half", "minus_half", "minus_zero"])
 @pytest.mark.parametrize("bzero", [0.0, -0.0], ids=["b_plus0", "b_minus0"])
 def test_all_ties_constant_logits(eqb, zbits, bzero):
