@@ -44,10 +44,16 @@
  * Errors.  Every argument check runs before anything is enqueued, so a call
  *   that returns an error has left the stream untouched.  T = 0 returns
  *   EQB_OK and enqueues nothing.
+ * Concurrency.  The library keeps no state between calls except a per-device
+ *   cache of the compute-unit count (filled once, thread-safe) and the
+ *   per-thread test cap of eqb_set_max_blocks.  Calls may be made from
+ *   several host threads and on several streams at once; calls that write
+ *   the same buffers must be ordered by the caller (same stream, or events).
  */
 #ifndef EQB_H
 #define EQB_H
 
+#include <stddef.h>
 #include <stdint.h>
 
 #ifdef __cplusplus
@@ -188,14 +194,17 @@ eqb_status eqb_select_uniform(const int32_t* hist, int32_t P, int32_t E, int32_t
  *   maxvio_global [1] binary64 (out): the whole batch, f_e = sum_p f_{p,e}, |B| = T
  *     ("Global MaxVio").
  *   maxvio_local [P] binary64 (out, nullable): partition p alone,
- *     |B| = part_off[p+1] - part_off[p] ("Local MaxVio"); NaN for an empty partition.
+ *     |B| = part_off[p+1] - part_off[p]; NaN for an empty partition.
+ *   maxvio_local_mean [1] binary64 (out, nullable): "Local MaxVio" as Appendix E
+ *     reports it, the per-partition values averaged over the non-empty
+ *     partitions (binary64 sum in ascending p, divided by their number).
  * Each value is (max_e f_e) * E / (K * |B|) - 1 in binary64: an exact integer
  * maximum, then one division and one subtraction, each rounded to nearest even.
  * T = 0 returns EQB_OK and writes nothing.
  */
 eqb_status eqb_max_violation(const int32_t* load, int64_t T, int32_t K, int32_t E,
                              const int64_t* part_off, int32_t P, double* maxvio_global,
-                             double* maxvio_local, void* stream);
+                             double* maxvio_local, double* maxvio_local_mean, void* stream);
 
 /*
  * Load-Error Injection, the residual (Sec. 4, Eq. lei and the normalisation
@@ -240,15 +249,56 @@ eqb_status eqb_lei_router_backward(const uint16_t* z, const int32_t* topk_idx, c
                                    int32_t P, float* grad_z, void* stream);
 
 /*
- * Tuning control (host only, no HIP call): caps the number of blocks of the
+ * One whole layer in one call (Sec. 2, Eq. 1 and "Quantile Balancing";
+ * Appendix C, Algorithm 1 steps 1-6; Eq. 2): routing with the fused coarse
+ * counts, the coarse selection, the fine counts and the fine selection with
+ * the centred bias, enqueued as five kernels on `stream`.  It computes what
+ * eqb_route_topk, eqb_select_quantile(1), eqb_margin_hist_pass2 and
+ * eqb_select_quantile(2) compute in sequence, with r = eqb_rank(T, K, E).
+ *   z [T,E] bf16 bits, b [E] binary32                       (in)
+ *   topk_idx [T,K] int32, topk_score [T,K] binary32, tau [T] (out)
+ *   load [P,E] int32                                         (out, WRITTEN: f_{p,e})
+ *   q_bf16 [E] (out: b_hat_e, BF16 bits), b_next [E] binary32 (out: Eq. 2)
+ *   hist_hi_sum, hist_lo_sum [E,256] int32 (nullable out): the summed coarse
+ *     counts H[e,u] and the summed fine counts L[e,v] inside u_e.
+ *   dev_status [1] int32 (out, WRITTEN): EQB_DEV_OK, or
+ *     EQB_DEV_RANK_EXCEEDS_COUNT when some expert's selection failed.
+ *   workspace: device memory of at least eqb_layer_workspace_size(E, P)
+ *     bytes, 256-byte aligned, owned by the caller.  It holds the
+ *     per-partition counts and the selections while the layer runs.  It must
+ *     be ALL ZERO when the call's work starts, and the call's work leaves it
+ *     all zero again (each selection clears the counts it has summed), so a
+ *     caller zeroes it once after allocating it and may then run layer after
+ *     layer with it.  After an error reported by the call or by the runtime
+ *     while its work ran, zero it again before the next use.  Two calls whose
+ *     work may overlap need two workspaces.
+ *   marks (nullable): host array of 5 hipEvent_t handles, each nullable,
+ *     recorded on `stream` before the route kernel, after it, after the
+ *     coarse selection, after the fine pass and after the last kernel (for
+ *     timing the stages of one layer without splitting the call).
+ * Returns EQB_ERR_RANK when T = 0 (no quantile), EQB_ERR_INVALID_ARG for a
+ * null pointer or a workspace that is too small, EQB_ERR_UNSUPPORTED for a
+ * misaligned z or workspace; other errors as for the calls it chains.
+ */
+size_t eqb_layer_workspace_size(int32_t E, int32_t P);   /* host only; 0 for unsupported E or P */
+eqb_status eqb_layer(const uint16_t* z, const float* b, int64_t T, int32_t E, int32_t K,
+                     const int64_t* part_off, int32_t P, int32_t* topk_idx, float* topk_score, float* tau,
+                     int32_t* load, uint16_t* q_bf16, float* b_next, int32_t* hist_hi_sum,
+                     int32_t* hist_lo_sum, int32_t* dev_status, void* workspace, size_t workspace_bytes,
+                     void* const* marks, void* stream);
+
+/*
+ * Test control (host only, no HIP call): caps the number of blocks of the
  * streaming kernels (routing, the margin passes, the LEI kernels) at
- * max_blocks for the calls that follow, in this process; 0 restores the
- * default (a whole number of blocks per compute unit).  Results do not
- * depend on it; tests use it to run one block, or a block count that does not
- * divide the rows, against the same oracle.  Negative values are
- * EQB_ERR_INVALID_ARG.
+ * max_blocks for the calls that follow FROM THE CALLING HOST THREAD; calls
+ * made from other threads keep their own setting (the default 0: a whole
+ * number of blocks per compute unit).  Results do not depend on it; tests
+ * use it to run one block, or a block count that does not divide the rows,
+ * against the same oracle.  Negative values are EQB_ERR_INVALID_ARG.
+ * eqb_get_max_blocks returns the calling thread's current cap.
  */
 eqb_status eqb_set_max_blocks(int32_t max_blocks);
+int32_t eqb_get_max_blocks(void);
 
 /* Host helper: r = ceil(T*K/E) (Sec. 3; the paper assumes T*K/E is an
  * integer), or -1 for invalid arguments.  Host only, no HIP call. */

@@ -10,7 +10,8 @@ Written from arXiv 2609.28053:
 * MaxVio (Sec. 5 and Appendix E, "Balance metrics"): for a token batch B,
   MaxVio(B) = max_e [ f_e(B) / fbar(B) - 1 ] with the uniform target
   fbar(B) = K|B|/E (Sec. 2).  Global MaxVio takes the loads of the whole
-  batch, Local MaxVio those of one local batch (a partition here).
+  batch; Local MaxVio is computed on each local batch (a partition here) and
+  then averaged over the local batches.
 * The closed QB loop (Eq. 2): the statistics of step q give the bias
   b^(q+1) that routes the batch of step q+1.
 * Load-Error Injection (Sec. 4, Eq. lei and the normalisation that bounds
@@ -90,6 +91,20 @@ def max_violation(load_pe, part_off, K: int):
     return glob, local
 
 
+def local_maxvio_mean(local) -> float:
+    """Local MaxVio as Appendix E reports it: the per-local-batch values
+    averaged over the local batches (empty partitions, which have no value,
+    are left out).  Binary64 sum in ascending partition order, divided by the
+    number of values; NaN when there is none."""
+    vals = [float(v) for v in np.asarray(local, np.float64) if not math.isnan(float(v))]
+    if not vals:
+        return float("nan")
+    acc = 0.0
+    for v in vals:
+        acc = acc + v
+    return acc / len(vals)
+
+
 # --------------------------------------------------------------------------
 # The closed QB loop (Eq. 2)
 # --------------------------------------------------------------------------
@@ -106,7 +121,7 @@ def qb_loop(batches, b0, K: int, part_off=None, threads: int = 1):
         res = _eqb.run_layer(z, b, K, off, threads=threads)
         glob, local = max_violation(res["load"], off, K)
         steps.append(dict(b=b.copy(), load=res["load"], maxvio_global=glob, maxvio_local=local,
-                          bhat=res["bhat"], b_next=res["b_next"]))
+                          maxvio_local_mean=local_maxvio_mean(local), bhat=res["bhat"], b_next=res["b_next"]))
         b = res["b_next"].astype(np.float32)
     return steps
 

@@ -5,12 +5,36 @@
 
 namespace eqb {
 
+// Maximum of f over the block (every thread receives it): within each wave,
+// then over the waves.
+__device__ __forceinline__ int64_t block_max_i64(int64_t f, int64_t* sh) {
+  for (int off = 32; off > 0; off >>= 1) {
+    const int64_t o = (int64_t)__shfl_xor((unsigned long long)f, off);
+    f = o > f ? o : f;
+  }
+  if ((threadIdx.x & 63) == 0) sh[threadIdx.x >> 6] = f;
+  __syncthreads();
+  int64_t m = sh[0];
+  for (int w = 1; w < (int)(blockDim.x >> 6); ++w) m = sh[w] > m ? sh[w] : m;
+  __syncthreads();
+  return m;
+}
+
+// MaxVio = (max_e f_e) * E / (K * |B|) - 1 in binary64: the integer maximum
+// is exact, the division and the subtraction round once each; NaN for an
+// empty batch.
+__device__ __forceinline__ double maxvio_of(int64_t m, int E, int K, int64_t n) {
+  return n > 0 ? (double)(m * E) / ((double)K * (double)n) - 1.0 : __builtin_nan("");
+}
+
 // Block p < P: partition p alone; block P: the whole batch (loads summed over
-// the partitions).  MaxVio = (max_e f_e) * E / (K * |B|) - 1 in binary64: the
-// integer maximum is exact, the division and the subtraction round once each.
+// the partitions) and, with out_local_mean, the mean of the partitions'
+// values over the non-empty partitions (Appendix E: Local MaxVio is computed
+// per local batch and then averaged), a binary64 sum in ascending partition
+// order divided by their number.
 __global__ __launch_bounds__(kNBins) void max_violation_kernel(
     const int32_t* __restrict__ load, int E, int K, const PartTable pt,
-    double* __restrict__ out_global, double* __restrict__ out_local) {
+    double* __restrict__ out_global, double* __restrict__ out_local, double* __restrict__ out_local_mean) {
   __shared__ int64_t sh_max[kNBins / 64];
   const int p = blockIdx.x;
   const int e = threadIdx.x;
@@ -22,29 +46,29 @@ __global__ __launch_bounds__(kNBins) void max_violation_kernel(
       for (int q = 0; q < pt.P; ++q) f += load[(int64_t)q * E + e];
     }
   }
-  // maximum over the block: within each wave, then over the waves
-  for (int off = 32; off > 0; off >>= 1) {
-    const int64_t o = (int64_t)__shfl_xor((unsigned long long)f, off);
-    f = o > f ? o : f;
+  const int64_t m = block_max_i64(f, sh_max);
+  const int64_t n = (p < pt.P) ? pt.off[p + 1] - pt.off[p] : pt.off[pt.P];
+  if (p < pt.P) {
+    if (e == 0 && out_local) out_local[p] = maxvio_of(m, E, K, n);
+    return;
   }
-  if ((e & 63) == 0) sh_max[e >> 6] = f;
-  __syncthreads();
-  if (e == 0) {
-    int64_t m = sh_max[0];
-    for (int w = 1; w < (int)(blockDim.x >> 6); ++w) m = sh_max[w] > m ? sh_max[w] : m;
-    const int64_t n = (p < pt.P) ? pt.off[p + 1] - pt.off[p] : pt.off[pt.P];
-    const double v = n > 0 ? (double)(m * E) / ((double)K * (double)n) - 1.0 : __builtin_nan("");
-    if (p < pt.P) {
-      if (out_local) out_local[p] = v;
-    } else {
-      *out_global = v;
-    }
+  if (e == 0) *out_global = maxvio_of(m, E, K, n);
+  if (out_local_mean == nullptr) return;
+  double acc = 0.0;
+  int count = 0;
+  for (int q = 0; q < pt.P; ++q) {
+    const int64_t nq = pt.off[q + 1] - pt.off[q];
+    if (nq == 0) continue;            // block-uniform
+    const int64_t mq = block_max_i64(e < E ? (int64_t)load[(int64_t)q * E + e] : 0, sh_max);
+    acc += maxvio_of(mq, E, K, nq);
+    ++count;
   }
+  if (e == 0) *out_local_mean = count > 0 ? acc / (double)count : __builtin_nan("");
 }
 
 eqb_status launch_max_violation(const int32_t* load, int E, int K, const PartTable& pt,
-                                double* out_global, double* out_local, hipStream_t s) {
-  max_violation_kernel<<<pt.P + 1, kNBins, 0, s>>>(load, E, K, pt, out_global, out_local);
+                                double* out_global, double* out_local, double* out_local_mean, hipStream_t s) {
+  max_violation_kernel<<<pt.P + 1, kNBins, 0, s>>>(load, E, K, pt, out_global, out_local, out_local_mean);
   return launch_status();
 }
 

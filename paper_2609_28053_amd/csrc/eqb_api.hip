@@ -6,23 +6,27 @@
 
 namespace eqb {
 
+// Compute units per device, queried once per device.  Concurrent first
+// calls may both query; they store the same value.
 int num_cus() {
-  static int cached[64] = {0};
+  static std::atomic<int> cached[64] = {};
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
-  if (cached[dev] == 0) {
-    int n = 0;
+  int n = cached[dev].load(std::memory_order_relaxed);
+  if (n <= 0) {
     if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
-    cached[dev] = n;
+    cached[dev].store(n, std::memory_order_relaxed);
   }
-  return cached[dev];
+  return n;
 }
 
 namespace {
-std::atomic<int> g_max_blocks{0};
+// Grid cap of eqb_set_max_blocks: per host thread, so a cap one caller sets
+// never changes the grids of calls made from other threads.
+thread_local int t_max_blocks = 0;
 }  // namespace
 
-int max_blocks_cap() { return g_max_blocks.load(std::memory_order_relaxed); }
+int max_blocks_cap() { return t_max_blocks; }
 
 namespace {
 
@@ -218,7 +222,7 @@ eqb_status eqb_select_uniform(const int32_t* hist, int32_t P, int32_t E, int32_t
 
 eqb_status eqb_max_violation(const int32_t* load, int64_t T, int32_t K, int32_t E,
                              const int64_t* part_off, int32_t P, double* maxvio_global,
-                             double* maxvio_local, void* stream) {
+                             double* maxvio_local, double* maxvio_local_mean, void* stream) {
   if (T < 0 || T > INT32_MAX || K < 1 || K >= E) return EQB_ERR_INVALID_ARG;
   if (!supported_E(E)) return EQB_ERR_UNSUPPORTED;
   PartTable pt;
@@ -226,7 +230,7 @@ eqb_status eqb_max_violation(const int32_t* load, int64_t T, int32_t K, int32_t 
   if (st != EQB_OK) return st;
   if (T == 0) return EQB_OK;
   if (!load || !maxvio_global) return EQB_ERR_INVALID_ARG;
-  return launch_max_violation(load, E, K, pt, maxvio_global, maxvio_local,
+  return launch_max_violation(load, E, K, pt, maxvio_global, maxvio_local, maxvio_local_mean,
                               static_cast<hipStream_t>(stream));
 }
 
@@ -271,11 +275,48 @@ eqb_status eqb_lei_router_backward(const uint16_t* z, const int32_t* topk_idx, c
                                     static_cast<hipStream_t>(stream));
 }
 
+size_t eqb_layer_workspace_size(int32_t E, int32_t P) {
+  if (!supported_E(E) || P < 1 || P > EQB_MAX_PARTITIONS) return 0;
+  return layer_workspace(nullptr, E, P, nullptr);
+}
+
+eqb_status eqb_layer(const uint16_t* z, const float* b, int64_t T, int32_t E, int32_t K,
+                     const int64_t* part_off, int32_t P, int32_t* topk_idx, float* topk_score, float* tau,
+                     int32_t* load, uint16_t* q_bf16, float* b_next, int32_t* hist_hi_sum,
+                     int32_t* hist_lo_sum, int32_t* dev_status, void* workspace, size_t workspace_bytes,
+                     void* const* marks, void* stream) {
+  if (T < 0 || T > INT32_MAX || K < 1 || K >= E) return EQB_ERR_INVALID_ARG;
+  if (!supported_E(E)) return EQB_ERR_UNSUPPORTED;
+  RouteArgs a;
+  const eqb_status st = make_table(part_off, P, T, &a.pt);
+  if (st != EQB_OK) return st;
+  const int64_t r = eqb_rank(T, K, E);
+  if (r < 1) return EQB_ERR_RANK;
+  if (!z || !b || !topk_idx || !topk_score || !tau || !load || !q_bf16 || !b_next || !dev_status || !workspace)
+    return EQB_ERR_INVALID_ARG;
+  if (!aligned16(z)) return EQB_ERR_UNSUPPORTED;
+  if (reinterpret_cast<uintptr_t>(workspace) % 256 != 0) return EQB_ERR_UNSUPPORTED;
+  LayerWorkspace w;
+  if (workspace_bytes < layer_workspace(workspace, E, a.pt.P, &w)) return EQB_ERR_INVALID_ARG;
+  a.z = z;
+  a.b = b;
+  a.T = T;
+  a.E = E;
+  a.K = K;
+  a.idx = topk_idx;
+  a.score = topk_score;
+  a.tau = tau;
+  return launch_layer(a, r, w, q_bf16, b_next, load, hist_hi_sum, hist_lo_sum, dev_status, marks,
+                      static_cast<hipStream_t>(stream));
+}
+
 eqb_status eqb_set_max_blocks(int32_t max_blocks) {
   if (max_blocks < 0) return EQB_ERR_INVALID_ARG;
-  g_max_blocks.store(max_blocks, std::memory_order_relaxed);
+  t_max_blocks = max_blocks;
   return EQB_OK;
 }
+
+int32_t eqb_get_max_blocks(void) { return t_max_blocks; }
 
 int64_t eqb_rank(int64_t T_total, int32_t K, int32_t E) {
   if (T_total < 0 || E < 1 || K < 1 || K >= E) return -1;

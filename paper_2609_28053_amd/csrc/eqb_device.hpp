@@ -245,6 +245,11 @@ __device__ __forceinline__ int64_t slab_sum(const int32_t* __restrict__ hist, in
   return c;
 }
 
+// Zeroes the P slabs of one counter (the layer form's consume-and-clear).
+__device__ __forceinline__ void slab_clear(int32_t* __restrict__ hist, int P, int64_t stride) {
+  for (int q = 0; q < P; ++q) hist[q * stride] = 0;
+}
+
 // ------------------------------------------------------- partition walk --
 // Calls f(p, s0, s1) for every piece of [r0, r1) lying in one partition and
 // holding at most kSegMax rows.  Uniform across the block.

@@ -37,6 +37,11 @@ eqb_status launch_select(int pass, const int32_t* hist, int P, int E, int64_t r,
                          int64_t* rank_in_bin, int32_t* sel_lo, uint16_t* q_bf16, float* b_next,
                          int32_t* hist_sum, int32_t* status, hipStream_t s);
 
+eqb_status launch_layer_selects(int pass, int32_t* hist, int P, int E, int64_t r, int32_t* sel_hi,
+                                int64_t* rank_in_bin, int32_t* sel_lo, uint16_t* q_bf16, float* b_next,
+                                int32_t* hist_sum, int32_t* load_acc, int32_t* load_out, int32_t* status,
+                                hipStream_t s);
+
 eqb_status launch_select_local(int pass, const int32_t* hist, int E, int K, const PartTable& pt,
                                int32_t* sel_hi, int64_t* rank_in_bin, int32_t* sel_lo, uint16_t* q_bf16,
                                int32_t* status, hipStream_t s);
@@ -47,7 +52,7 @@ eqb_status launch_uniform_hist(const uint16_t* z, const float* tau, int64_t T, i
 eqb_status launch_select_uniform(const int32_t* hist, int P, int E, int nbins, int64_t r, double lo,
                                  double width, double* est, float* b_next, int32_t* status, hipStream_t s);
 eqb_status launch_max_violation(const int32_t* load, int E, int K, const PartTable& pt,
-                                double* out_global, double* out_local, hipStream_t s);
+                                double* out_global, double* out_local, double* out_local_mean, hipStream_t s);
 
 eqb_status launch_lei_residual(const int32_t* load, int E, int K, const PartTable& pt, double eta,
                                double c, float* inj, hipStream_t s);
@@ -55,6 +60,51 @@ eqb_status launch_lei_router_backward(const uint16_t* z, const int32_t* idx, con
                                       int64_t T, int E, int K, float* gz, const PartTable& pt, hipStream_t s);
 eqb_status launch_lei_inject(float* grad, const float* inj, int64_t T, int E, const PartTable& pt,
                              hipStream_t s);
+
+// Working buffers of one layer (eqb_layer): the per-partition coarse and
+// fine counts, the loads as the route kernel accumulates them, and the
+// selections.  Each piece starts on a 256-byte boundary.  The counters are
+// zero when a layer starts and zero again when it ends: the selection that
+// reads a counter clears it.
+struct LayerWorkspace {
+  int32_t* hist_hi;       // [P,E,256]
+  int32_t* hist_lo;       // [P,E,256]
+  int32_t* load_acc;      // [P,E]
+  int32_t* sel_hi;        // [E]
+  int32_t* sel_lo;        // [E]
+  int64_t* rank_in_bin;   // [E]
+};
+
+inline size_t align256(size_t n) { return (n + 255) & ~(size_t)255; }
+
+// Bytes of a layer workspace, and its pieces carved from base (null base:
+// only the size is computed).
+inline size_t layer_workspace(void* base, int E, int P, LayerWorkspace* w) {
+  const size_t hist = align256((size_t)P * E * kNBins * sizeof(int32_t));
+  const size_t load = align256((size_t)P * E * sizeof(int32_t));
+  const size_t sel = align256((size_t)E * sizeof(int32_t));
+  const size_t rib = align256((size_t)E * sizeof(int64_t));
+  if (base && w) {
+    char* p = static_cast<char*>(base);
+    w->hist_hi = reinterpret_cast<int32_t*>(p);
+    w->hist_lo = reinterpret_cast<int32_t*>(p + hist);
+    w->load_acc = reinterpret_cast<int32_t*>(p + 2 * hist);
+    w->sel_hi = reinterpret_cast<int32_t*>(p + 2 * hist + load);
+    w->sel_lo = reinterpret_cast<int32_t*>(p + 2 * hist + load + sel);
+    w->rank_in_bin = reinterpret_cast<int64_t*>(p + 2 * hist + load + 2 * sel);
+  }
+  return 2 * hist + load + 2 * sel + rib;
+}
+
+// The whole layer on one stream: route + loads + coarse counts, coarse
+// selection (clearing the coarse counts, handing the loads out), fine
+// counts, fine selection (clearing the fine counts), centring and status.
+// marks (nullable, 5 entries, each nullable): events recorded before the
+// route kernel, after it, after the coarse selection, after the fine pass
+// and at the end.
+eqb_status launch_layer(const RouteArgs& route, int64_t r, const LayerWorkspace& w, uint16_t* q_bf16,
+                        float* b_next, int32_t* load_out, int32_t* hist_hi_sum, int32_t* hist_lo_sum,
+                        int32_t* dev_status, void* const* marks, hipStream_t s);
 
 // Number of compute units of the current device (cached per device).
 int num_cus();

@@ -11,11 +11,16 @@ namespace eqb {
 // the whole batch.  kLocal: slab p alone, with its own rank
 // r_p = ceil(|B_p| K / E), written to entry [p, e]; an empty partition has no
 // quantile and gets -1 without raising the status.
+// Layer form (eqb_layer): `clear` zeroes the summed counters once read, and
+// the loads accumulated by the route kernel (load_acc [P,E]) are copied to
+// load_out and zeroed, so the workspace is left as it was found: all zero.
+// Each counter is read and cleared by the same thread.
 template <bool kLocal>
 __global__ __launch_bounds__(kNBins) void select_coarse_kernel(
-    const int32_t* __restrict__ hist, int P, int E, int K, int64_t r, const PartTable pt,
+    int32_t* __restrict__ hist, int P, int E, int K, int64_t r, const PartTable pt,
     int32_t* __restrict__ sel_hi, int64_t* __restrict__ rank_in_bin, int32_t* __restrict__ hist_sum,
-    int32_t* __restrict__ status) {
+    int32_t* __restrict__ status, bool clear = false, int32_t* __restrict__ load_acc = nullptr,
+    int32_t* __restrict__ load_out = nullptr) {
   __shared__ int64_t sh[kNBins];
   const int e = blockIdx.x, u = threadIdx.x, p = kLocal ? (int)blockIdx.y : 0;
   const int64_t out = kLocal ? (int64_t)p * E + e : e;
@@ -36,6 +41,13 @@ __global__ __launch_bounds__(kNBins) void select_coarse_kernel(
   } else {
     c = slab_sum(hist + (int64_t)e * kNBins + u, P, (int64_t)E * kNBins);
     if (hist_sum) hist_sum[(int64_t)e * kNBins + u] = (int32_t)c;
+    if (clear) slab_clear(hist + (int64_t)e * kNBins + u, P, (int64_t)E * kNBins);
+    if (load_acc) {
+      for (int q = u; q < P; q += kNBins) {
+        load_out[(int64_t)q * E + e] = load_acc[(int64_t)q * E + e];
+        load_acc[(int64_t)q * E + e] = 0;
+      }
+    }
   }
   const int64_t cum = block_inclusive_scan_256(c, sh);
   if (cum >= r && cum - c < r) {
@@ -51,9 +63,10 @@ __global__ __launch_bounds__(kNBins) void select_coarse_kernel(
 
 template <bool kLocal>
 __global__ __launch_bounds__(kNBins) void select_fine_kernel(
-    const int32_t* __restrict__ hist, int P, int E, const PartTable pt, const int32_t* __restrict__ sel_hi,
+    int32_t* __restrict__ hist, int P, int E, const PartTable pt, const int32_t* __restrict__ sel_hi,
     const int64_t* __restrict__ rank_in_bin, int32_t* __restrict__ sel_lo,
-    uint16_t* __restrict__ q_bf16, int32_t* __restrict__ hist_sum, int32_t* __restrict__ status) {
+    uint16_t* __restrict__ q_bf16, int32_t* __restrict__ hist_sum, int32_t* __restrict__ status,
+    bool clear = false) {
   __shared__ int64_t sh[kNBins];
   const int e = blockIdx.x, v = threadIdx.x, p = kLocal ? (int)blockIdx.y : 0;
   const int64_t out = kLocal ? (int64_t)p * E + e : e;
@@ -73,6 +86,7 @@ __global__ __launch_bounds__(kNBins) void select_fine_kernel(
   } else {
     c = slab_sum(hist + (int64_t)e * kNBins + v, P, (int64_t)E * kNBins);
     if (hist_sum) hist_sum[(int64_t)e * kNBins + v] = (int32_t)c;
+    if (clear) slab_clear(hist + (int64_t)e * kNBins + v, P, (int64_t)E * kNBins);
   }
   const int64_t cum = block_inclusive_scan_256(c, sh);
   const bool ok = u >= 0 && u < kNBins && rho >= 1;
@@ -88,20 +102,94 @@ __global__ __launch_bounds__(kNBins) void select_fine_kernel(
 }
 
 // b = b_hat - mean(b_hat): binary64 sum in ascending expert order, divided by
-// E, difference in binary64, one rounding to binary32.
+// E, difference in binary64, one rounding to binary32.  With status_out (the
+// layer form) the kernel also writes the layer's status (an expert whose fine
+// selection failed, sel_lo = -1, holds fewer counts than its rank) and, as the
+// layer's last kernel, zeroes the selections it leaves behind in the
+// workspace (sel_hi, rank_in_bin, sel_lo), each by the thread that read it.
 __global__ __launch_bounds__(256) void center_kernel(const uint16_t* __restrict__ q, int E,
-                                                     float* __restrict__ b_next) {
+                                                     float* __restrict__ b_next,
+                                                     int32_t* __restrict__ sel_lo = nullptr,
+                                                     int32_t* __restrict__ status_out = nullptr,
+                                                     int32_t* __restrict__ sel_hi = nullptr,
+                                                     int64_t* __restrict__ rank_in_bin = nullptr) {
   __shared__ double val[256];
   __shared__ double mean;
   for (int e = threadIdx.x; e < E; e += blockDim.x) val[e] = (double)__uint_as_float((uint32_t)q[e] << 16);
-  __syncthreads();
+  int bad = 0;
+  if (status_out) {
+    for (int e = threadIdx.x; e < E; e += blockDim.x) {
+      bad |= (int)(sel_lo[e] < 0);
+      sel_lo[e] = 0;
+      sel_hi[e] = 0;
+      rank_in_bin[e] = 0;
+    }
+  }
+  bad = __syncthreads_or(bad);
   if (threadIdx.x == 0) {
     double acc = 0.0;
     for (int e = 0; e < E; ++e) acc += val[e];
     mean = acc / (double)E;
+    if (status_out) *status_out = bad ? EQB_DEV_RANK_EXCEEDS_COUNT : EQB_DEV_OK;
   }
   __syncthreads();
   for (int e = threadIdx.x; e < E; e += blockDim.x) b_next[e] = (float)(val[e] - mean);
+}
+
+eqb_status launch_layer_selects(int pass, int32_t* hist, int P, int E, int64_t r, int32_t* sel_hi,
+                                int64_t* rank_in_bin, int32_t* sel_lo, uint16_t* q_bf16, float* b_next,
+                                int32_t* hist_sum, int32_t* load_acc, int32_t* load_out, int32_t* status,
+                                hipStream_t s) {
+  PartTable none{};
+  none.P = P;
+  if (pass == 1) {
+    select_coarse_kernel<false><<<E, kNBins, 0, s>>>(hist, P, E, 0, r, none, sel_hi, rank_in_bin, hist_sum,
+                                                     nullptr, true, load_acc, load_out);
+    return launch_status();
+  }
+  select_fine_kernel<false><<<E, kNBins, 0, s>>>(hist, P, E, none, sel_hi, rank_in_bin, sel_lo, q_bf16,
+                                                 hist_sum, nullptr, true);
+  if (launch_status() != EQB_OK) return EQB_ERR_HIP;
+  center_kernel<<<1, 256, 0, s>>>(q_bf16, E, b_next, sel_lo, status, sel_hi, rank_in_bin);
+  return launch_status();
+}
+
+static eqb_status mark(void* const* marks, int i, hipStream_t s) {
+  if (marks == nullptr || marks[i] == nullptr) return EQB_OK;
+  return hipEventRecord(static_cast<hipEvent_t>(marks[i]), s) == hipSuccess ? EQB_OK : EQB_ERR_HIP;
+}
+
+eqb_status launch_layer(const RouteArgs& route, int64_t r, const LayerWorkspace& w, uint16_t* q_bf16,
+                        float* b_next, int32_t* load_out, int32_t* hist_hi_sum, int32_t* hist_lo_sum,
+                        int32_t* dev_status, void* const* marks, hipStream_t s) {
+  RouteArgs a = route;
+  a.load = w.load_acc;
+  a.hist = w.hist_hi;
+  eqb_status st = mark(marks, 0, s);
+  if (st != EQB_OK) return st;
+  st = launch_route(a, s);
+  if (st != EQB_OK) return st;
+  if ((st = mark(marks, 1, s)) != EQB_OK) return st;
+  const int P = a.pt.P, E = a.E;
+  st = launch_layer_selects(1, w.hist_hi, P, E, r, w.sel_hi, w.rank_in_bin, nullptr, nullptr, nullptr,
+                            hist_hi_sum, w.load_acc, load_out, nullptr, s);
+  if (st != EQB_OK) return st;
+  if ((st = mark(marks, 2, s)) != EQB_OK) return st;
+  MarginArgs m;
+  m.z = a.z;
+  m.tau = a.tau;
+  m.T = a.T;
+  m.E = E;
+  m.sel_hi = w.sel_hi;
+  m.hist = w.hist_lo;
+  m.pt = a.pt;
+  st = launch_margin(true, m, s);
+  if (st != EQB_OK) return st;
+  if ((st = mark(marks, 3, s)) != EQB_OK) return st;
+  st = launch_layer_selects(2, w.hist_lo, P, E, r, w.sel_hi, w.rank_in_bin, w.sel_lo, q_bf16, b_next,
+                            hist_lo_sum, nullptr, nullptr, dev_status, s);
+  if (st != EQB_OK) return st;
+  return mark(marks, 4, s);
 }
 
 eqb_status launch_select(int pass, const int32_t* hist, int P, int E, int64_t r, int32_t* sel_hi,
@@ -110,12 +198,12 @@ eqb_status launch_select(int pass, const int32_t* hist, int P, int E, int64_t r,
   PartTable none{};
   none.P = P;
   if (pass == 1) {
-    select_coarse_kernel<false><<<E, kNBins, 0, s>>>(hist, P, E, 0, r, none, sel_hi, rank_in_bin, hist_sum,
-                                                     status);
+    select_coarse_kernel<false><<<E, kNBins, 0, s>>>(const_cast<int32_t*>(hist), P, E, 0, r, none, sel_hi,
+                                                     rank_in_bin, hist_sum, status);
     return launch_status();
   }
-  select_fine_kernel<false><<<E, kNBins, 0, s>>>(hist, P, E, none, sel_hi, rank_in_bin, sel_lo, q_bf16,
-                                                 hist_sum, status);
+  select_fine_kernel<false><<<E, kNBins, 0, s>>>(const_cast<int32_t*>(hist), P, E, none, sel_hi, rank_in_bin,
+                                                 sel_lo, q_bf16, hist_sum, status);
   if (launch_status() != EQB_OK) return EQB_ERR_HIP;
   if (b_next) {
     center_kernel<<<1, 256, 0, s>>>(q_bf16, E, b_next);
@@ -129,11 +217,11 @@ eqb_status launch_select_local(int pass, const int32_t* hist, int E, int K, cons
                                int32_t* status, hipStream_t s) {
   const dim3 grid(E, pt.P);
   if (pass == 1)
-    select_coarse_kernel<true><<<grid, kNBins, 0, s>>>(hist, pt.P, E, K, 0, pt, sel_hi, rank_in_bin, nullptr,
-                                                       status);
+    select_coarse_kernel<true><<<grid, kNBins, 0, s>>>(const_cast<int32_t*>(hist), pt.P, E, K, 0, pt, sel_hi,
+                                                       rank_in_bin, nullptr, status);
   else
-    select_fine_kernel<true><<<grid, kNBins, 0, s>>>(hist, pt.P, E, pt, sel_hi, rank_in_bin, sel_lo, q_bf16,
-                                                     nullptr, status);
+    select_fine_kernel<true><<<grid, kNBins, 0, s>>>(const_cast<int32_t*>(hist), pt.P, E, pt, sel_hi,
+                                                     rank_in_bin, sel_lo, q_bf16, nullptr, status);
   return launch_status();
 }
 

@@ -43,7 +43,10 @@ EXPORTS = (
     "eqb_lei_residual",
     "eqb_lei_inject",
     "eqb_lei_router_backward",
+    "eqb_layer_workspace_size",
+    "eqb_layer",
     "eqb_set_max_blocks",
+    "eqb_get_max_blocks",
     "eqb_rank",
     "eqb_status_string",
 )
@@ -69,11 +72,14 @@ def _load():
         "eqb_rank_average": [P, i64, i32, P, i32, P, P, P],
         "eqb_margin_hist_uniform": [P, P, i64, i32, P, i32, ctypes.c_float, ctypes.c_float, i32, P, P],
         "eqb_select_uniform": [P, i32, i32, i32, i64, ctypes.c_float, ctypes.c_float, P, P, P, P],
-        "eqb_max_violation": [P, i64, i32, i32, P, i32, P, P, P],
+        "eqb_max_violation": [P, i64, i32, i32, P, i32, P, P, P, P],
         "eqb_lei_residual": [P, i64, i32, i32, P, i32, ctypes.c_double, ctypes.c_double, P, P],
         "eqb_lei_inject": [P, P, i64, i32, P, i32, P],
         "eqb_lei_router_backward": [P, P, P, P, i64, i32, i32, P, i32, P, P],
+        "eqb_layer_workspace_size": [i32, i32],
+        "eqb_layer": [P, P, i64, i32, i32, P, i32, P, P, P, P, P, P, P, P, P, P, ctypes.c_size_t, P, P],
         "eqb_set_max_blocks": [i32],
+        "eqb_get_max_blocks": [],
         "eqb_rank": [i64, i32, i32],
         "eqb_status_string": [i32],
     }
@@ -82,6 +88,7 @@ def _load():
         fn.argtypes = args
         fn.restype = i32
     lib.eqb_rank.restype = i64
+    lib.eqb_layer_workspace_size.restype = ctypes.c_size_t
     lib.eqb_status_string.restype = ctypes.c_char_p
     return lib
 
@@ -122,9 +129,23 @@ def _stream(stream) -> ctypes.c_void_p:
     return ctypes.c_void_p(stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream))
 
 
-def _offsets(part_off: Optional[Sequence[int]], T: int):
+class PartOffsets:
+    """A partition table converted once for repeated calls: P+1 token
+    offsets held as an int64 array with its pointer ready for the C ABI."""
+
+    __slots__ = ("arr", "ptr", "P")
+
+    def __init__(self, part_off: Sequence[int]):
+        self.arr = np.ascontiguousarray(np.asarray(part_off, dtype=np.int64))
+        self.ptr = self.arr.ctypes.data_as(ctypes.c_void_p)
+        self.P = self.arr.size - 1
+
+
+def _offsets(part_off, T: int):
     if part_off is None:
         return None, 1, None
+    if isinstance(part_off, PartOffsets):
+        return part_off.ptr, part_off.P, part_off
     arr = np.ascontiguousarray(np.asarray(part_off, dtype=np.int64))
     P = arr.size - 1
     return arr.ctypes.data_as(ctypes.c_void_p), P, arr     # keep arr alive
@@ -242,7 +263,8 @@ def eqb_select_uniform(hist, r, lo, hi, est, b_next=None, dev_status=None, strea
         _ptr(dev_status, torch.int32, 1, "dev_status"), _stream(stream)))
 
 
-def eqb_max_violation(load, T, K, maxvio_global, maxvio_local=None, part_off=None, stream=None):
+def eqb_max_violation(load, T, K, maxvio_global, maxvio_local=None, part_off=None, maxvio_local_mean=None,
+                      stream=None):
     P, E = load.shape
     po, Pn, keep = _offsets(part_off, T)
     if Pn != P:
@@ -250,7 +272,8 @@ def eqb_max_violation(load, T, K, maxvio_global, maxvio_local=None, part_off=Non
     _check("eqb_max_violation", lib.eqb_max_violation(
         _ptr(load, torch.int32, P * E, "load"), T, K, E, po, P,
         _ptr(maxvio_global, torch.float64, 1, "maxvio_global"),
-        _ptr(maxvio_local, torch.float64, P, "maxvio_local"), _stream(stream)))
+        _ptr(maxvio_local, torch.float64, P, "maxvio_local"),
+        _ptr(maxvio_local_mean, torch.float64, 1, "maxvio_local_mean"), _stream(stream)))
     del keep
 
 
@@ -285,8 +308,49 @@ def eqb_lei_router_backward(z, topk_idx, grad_score, grad_z, inj=None, part_off=
     del keep
 
 
+def eqb_layer_workspace_size(E: int, P: int) -> int:
+    return int(lib.eqb_layer_workspace_size(E, P))
+
+
+def layer_marks(events):
+    """The marks argument of eqb_layer from five torch.cuda.Event objects (or
+    None entries).  An event's handle exists once it has been recorded, so
+    each is recorded once here first."""
+    handles = []
+    for ev in events:
+        if ev is None:
+            handles.append(None)
+            continue
+        if not ev.cuda_event:
+            ev.record()
+        handles.append(ev.cuda_event)
+    return (ctypes.c_void_p * 5)(*handles)
+
+
+def eqb_layer(z, b, K, topk_idx, topk_score, tau, load, q_bf16, b_next, dev_status, workspace,
+              part_off=None, hist_hi_sum=None, hist_lo_sum=None, marks=None, stream=None):
+    T, E = z.shape
+    po, P, keep = _offsets(part_off, T)
+    _check("eqb_layer", lib.eqb_layer(
+        _ptr(z, _Z, name="z"), _ptr(b, torch.float32, E, "b"), T, E, K, po, P,
+        _ptr(topk_idx, torch.int32, T * K, "topk_idx"), _ptr(topk_score, torch.float32, T * K, "topk_score"),
+        _ptr(tau, torch.float32, T, "tau"), _ptr(load, torch.int32, P * E, "load"),
+        _ptr(q_bf16, _Z, E, "q_bf16"), _ptr(b_next, torch.float32, E, "b_next"),
+        _ptr(hist_hi_sum, torch.int32, E * EQB_NBINS, "hist_hi_sum"),
+        _ptr(hist_lo_sum, torch.int32, E * EQB_NBINS, "hist_lo_sum"),
+        _ptr(dev_status, torch.int32, 1, "dev_status"), _ptr(workspace, torch.uint8, name="workspace"),
+        workspace.numel(), marks, _stream(stream)))
+    del keep
+
+
 def eqb_set_max_blocks(max_blocks: int) -> None:
+    """Test control: caps the streaming kernels' grids for calls made later
+    from the calling thread only."""
     _check("eqb_set_max_blocks", lib.eqb_set_max_blocks(int(max_blocks)))
+
+
+def eqb_get_max_blocks() -> int:
+    return int(lib.eqb_get_max_blocks())
 
 
 def eqb_rank(T_total: int, K: int, E: int) -> int:
@@ -318,6 +382,35 @@ class Layer:
         self.rank_in_bin = torch.empty(E, dtype=torch.int64, device=dev)
         self.q_bf16 = torch.empty(E, dtype=torch.int16, device=dev)
         self.b_next = torch.empty(E, dtype=torch.float32, device=dev)
+
+    def _layer_buffers(self):
+        """Buffers of the one-call layer (eqb_layer): a workspace, zeroed once
+        here and left zeroed by every call, and the outputs it writes."""
+        if getattr(self, "workspace", None) is None:
+            dev = self.topk_idx.device
+            n = eqb_layer_workspace_size(self.E, self.P)
+            self.workspace = torch.zeros(n, dtype=torch.uint8, device=dev)
+            self.load_out = torch.empty((self.P, self.E), dtype=torch.int32, device=dev)
+            self.status = torch.empty(1, dtype=torch.int32, device=dev)
+
+    def step(self, z, b, part_off=None, sums=False, marks=None, stream=None):
+        """One layer through eqb_layer: one C call, five kernels, no fill of
+        counters (the workspace comes back zeroed).  Writes topk_idx,
+        topk_score, tau, load_out, q_bf16, b_next, status and, with sums=True,
+        the summed counts H and L.  marks: see layer_marks."""
+        self._layer_buffers()
+        eqb_layer(z, b, self.K, self.topk_idx, self.topk_score, self.tau, self.load_out, self.q_bf16,
+                  self.b_next, self.status, self.workspace, part_off,
+                  self.H if sums else None, self.L if sums else None, marks, stream)
+        return self
+
+    def step_results(self) -> dict:
+        """Host copies of the one-call layer's outputs (synchronises)."""
+        torch.cuda.synchronize()
+        g = lambda t: t.cpu().numpy()
+        return dict(idx=g(self.topk_idx), score=g(self.topk_score), tau=g(self.tau), load=g(self.load_out),
+                    H=g(self.H), L=g(self.L), bhat=g(self.q_bf16).view(np.uint16), b_next=g(self.b_next),
+                    dev_status=int(self.status.item()), workspace_zero=bool((self.workspace == 0).all().item()))
 
     def run(self, z, b, part_off=None, fused=True, stream=None):
         """One layer: route (+ coarse counts), select 1, fine counts, select 2."""
@@ -375,16 +468,18 @@ def qb_loop(batches, b0, K: int, part_off=None, stream=None):
         lay = Layer(T, E, K, P, device=dev)
         mv_g = torch.empty(1, dtype=torch.float64, device=dev)
         mv_l = torch.empty(P, dtype=torch.float64, device=dev)
+        mv_m = torch.empty(1, dtype=torch.float64, device=dev)
         b = b0.detach().to(device=dev, dtype=torch.float32).clone()
         for z in batches:
             if tuple(z.shape) != (T, E):
                 raise ValueError("every batch of the loop has the same shape")
             lay.run(z, b, part_off)
-            eqb_max_violation(lay.load, T, K, mv_g, mv_l, part_off)
+            eqb_max_violation(lay.load, T, K, mv_g, mv_l, part_off, mv_m)
             b_used = b.clone()
             b.copy_(lay.b_next)
             steps.append(dict(b=b_used.cpu().numpy(), load=lay.load.cpu().numpy(),
                               maxvio_global=float(mv_g.item()), maxvio_local=mv_l.cpu().numpy(),
+                              maxvio_local_mean=float(mv_m.item()),
                               bhat=lay.q_bf16.cpu().numpy().view(np.uint16), b_next=b.cpu().numpy(),
                               dev_status=int(lay.dev_status.item())))
     return steps

@@ -30,11 +30,15 @@ def lib():
     lib.eqb_margin_hist_pass2.argtypes = [V, V, i64, i32, V, V, i32, V, V]
     lib.eqb_select_quantile.argtypes = [i32, V, i32, i32, i64, V, V, V, V, V, V, V, V]
     lib.eqb_expert_load.argtypes = [V, i64, i32, i32, V, i32, V, V]
-    lib.eqb_max_violation.argtypes = [V, i64, i32, i32, V, i32, V, V, V]
+    lib.eqb_max_violation.argtypes = [V, i64, i32, i32, V, i32, V, V, V, V]
     lib.eqb_lei_residual.argtypes = [V, i64, i32, i32, V, i32, ctypes.c_double, ctypes.c_double, V, V]
     lib.eqb_lei_inject.argtypes = [V, V, i64, i32, V, i32, V]
     lib.eqb_lei_router_backward.argtypes = [V, V, V, V, i64, i32, i32, V, i32, V, V]
+    lib.eqb_layer_workspace_size.argtypes = [i32, i32]
+    lib.eqb_layer_workspace_size.restype = ctypes.c_size_t
+    lib.eqb_layer.argtypes = [V, V, i64, i32, i32, V, i32] + [V] * 10 + [ctypes.c_size_t, V, V]
     lib.eqb_set_max_blocks.argtypes = [i32]
+    lib.eqb_get_max_blocks.argtypes = []
     lib.eqb_rank.argtypes = [i64, i32, i32]
     lib.eqb_rank.restype = i64
     lib.eqb_status_string.argtypes = [i32]
@@ -130,14 +134,14 @@ def test_select_checks(lib):
 
 def test_max_violation_checks(lib):
     m = lib.eqb_max_violation
-    assert m(FAKE, 64, 0, 8, None, 1, FAKE, None, None) == INVALID        # K < 1
-    assert m(FAKE, 64, 8, 8, None, 1, FAKE, None, None) == INVALID        # K >= E
-    assert m(FAKE, 64, 2, 12, None, 1, FAKE, None, None) == UNSUPPORTED
-    assert m(None, 64, 2, 8, None, 1, FAKE, None, None) == INVALID
-    assert m(FAKE, 64, 2, 8, None, 1, None, None, None) == INVALID        # no global output
+    assert m(FAKE, 64, 0, 8, None, 1, FAKE, None, None, None) == INVALID        # K < 1
+    assert m(FAKE, 64, 8, 8, None, 1, FAKE, None, None, None) == INVALID        # K >= E
+    assert m(FAKE, 64, 2, 12, None, 1, FAKE, None, None, None) == UNSUPPORTED
+    assert m(None, 64, 2, 8, None, 1, FAKE, None, None, None) == INVALID
+    assert m(FAKE, 64, 2, 8, None, 1, None, None, None, None) == INVALID        # no global output
     po, keep = offs(0, 10, 5, 64)
-    assert m(FAKE, 64, 2, 8, po, 3, FAKE, FAKE, None) == INVALID          # decreasing offsets
-    assert m(FAKE, 0, 2, 8, None, 1, FAKE, None, None) == OK              # empty batch
+    assert m(FAKE, 64, 2, 8, po, 3, FAKE, FAKE, None, None) == INVALID          # decreasing offsets
+    assert m(FAKE, 0, 2, 8, None, 1, FAKE, None, None, None) == OK              # empty batch
 
 
 def test_lei_checks(lib):
@@ -184,3 +188,56 @@ def test_rank_and_status_strings(lib):
     assert lib.eqb_status_string(0) == b"EQB_OK"
     assert lib.eqb_status_string(3) == b"EQB_ERR_RANK"
     assert lib.eqb_status_string(99) == b"EQB_ERR_UNKNOWN"
+
+
+def layer(lib, T=64, E=8, K=2, ws=ctypes.c_void_p(0x10000), ws_bytes=1 << 30, po=None, P=1, z=FAKE):
+    return lib.eqb_layer(z, FAKE, T, E, K, po, P, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, None, FAKE,
+                         ws, ws_bytes, None, None)
+
+
+def test_layer_workspace_size(lib):
+    # two [P,E,256] int32 count slabs, the [P,E] loads and three [E] selections,
+    # each rounded up to 256 bytes
+    for E, P in ((8, 1), (64, 4), (256, 16), (256, 256)):
+        want = 2 * P * E * 1024 + -(-4 * P * E // 256) * 256 + 2 * -(-4 * E // 256) * 256 + -(-8 * E // 256) * 256
+        assert lib.eqb_layer_workspace_size(E, P) == want
+    assert lib.eqb_layer_workspace_size(12, 1) == 0
+    assert lib.eqb_layer_workspace_size(8, 0) == 0
+    assert lib.eqb_layer_workspace_size(8, 257) == 0
+
+
+def test_layer_argument_checks(lib):
+    assert layer(lib, T=0) == RANK                                 # no margins, no quantile
+    assert layer(lib, K=8) == INVALID
+    assert layer(lib, E=12) == UNSUPPORTED
+    assert layer(lib, ws=None) == INVALID
+    assert layer(lib, ws=ctypes.c_void_p(0x10010)) == UNSUPPORTED   # not 256-byte aligned
+    assert layer(lib, ws_bytes=lib.eqb_layer_workspace_size(8, 1) - 1) == INVALID
+    assert layer(lib, z=ctypes.c_void_p(0x10002)) == UNSUPPORTED
+    po, keep = offs(0, 10, 64)
+    assert layer(lib, po=po, P=2, ws_bytes=lib.eqb_layer_workspace_size(8, 1)) == INVALID   # sized for P=1
+    bad, keep2 = offs(0, 70, 64)
+    assert layer(lib, po=bad, P=2) == INVALID
+
+
+def test_grid_cap_is_per_thread(lib):
+    """A cap set on one host thread leaves other threads' grids alone."""
+    import threading
+    assert lib.eqb_set_max_blocks(3) == OK
+    seen = {}
+
+    def other():
+        seen["before"] = lib.eqb_get_max_blocks()
+        lib.eqb_set_max_blocks(7)
+        seen["after"] = lib.eqb_get_max_blocks()
+
+    t = threading.Thread(target=other)
+    t.start()
+    t.join()
+    try:
+        assert seen == {"before": 0, "after": 7}
+        assert lib.eqb_get_max_blocks() == 3
+    finally:
+        assert lib.eqb_set_max_blocks(0) == OK
+    assert lib.eqb_set_max_blocks(-1) == INVALID
+

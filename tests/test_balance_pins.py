@@ -73,6 +73,42 @@ def test_local_maxvio_uses_the_partition_size():
     assert glob == pytest.approx(110 / (2 * 110 / 8) - 1)
 
 
+def test_local_maxvio_is_the_mean_over_local_batches():
+    """Appendix E: Local MaxVio is computed per local batch and then averaged.
+    Hand case (E = 8, K = 2): partition 0 has 10 tokens (uniform load 2.5)
+    and a largest load of 10, MaxVio 3; partition 1 is empty (no value);
+    partition 2 has 100 tokens (uniform 25) and a largest load of 50,
+    MaxVio 1.  Local MaxVio = (3 + 1) / 2 = 2, while the largest local value
+    is 3 and Global MaxVio (110 tokens, largest load 60) is 60/27.5 - 1."""
+    load = np.array([[10, 6, 4, 0, 0, 0, 0, 0],
+                     [0, 0, 0, 0, 0, 0, 0, 0],
+                     [50, 40, 30, 30, 20, 10, 10, 10]])
+    off = [0, 10, 10, 110]
+    glob, local = B.max_violation(load, off, 2)
+    assert local[0] == 3.0 and math.isnan(local[1]) and local[2] == 1.0
+    assert B.local_maxvio_mean(local) == 2.0
+    assert float(Fraction(60) / Fraction(2 * 110, 8) - 1) == pytest.approx(glob, rel=1e-15)
+    assert math.isnan(B.local_maxvio_mean([float("nan")]))
+    # mean over many partitions against exact rationals
+    rng = np.random.default_rng(12)
+    vals = rng.standard_normal(37)
+    want = sum(Fraction(float(v)) for v in vals) / 37
+    assert B.local_maxvio_mean(vals) == pytest.approx(float(want), rel=1e-14)
+
+
+@pytest.mark.parametrize("mutant", ["max", "empty_as_zero"])
+def test_local_mean_pins_catch_planted_mistakes(monkeypatch, mutant):
+    orig = B.local_maxvio_mean
+    if mutant == "max":
+        bad = lambda local: float(np.nanmax(np.asarray(local, np.float64)))
+    else:
+        bad = lambda local: float(np.mean(np.nan_to_num(np.asarray(local, np.float64), nan=0.0)))
+    monkeypatch.setattr(B, "local_maxvio_mean", bad)
+    with pytest.raises(AssertionError):
+        test_local_maxvio_is_the_mean_over_local_batches()
+    monkeypatch.setattr(B, "local_maxvio_mean", orig)
+
+
 def test_qb_loop_balances_fresh_batches():
     """Eq. 2's purpose: the bias from step q balances step q+1's batch."""
     w = W.WORKLOADS["skew64"].with_T(32768, 4)

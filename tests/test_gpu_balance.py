@@ -44,11 +44,13 @@ def test_max_violation_matches_oracle(eqb, E, P):
     lt = torch.from_numpy(load).cuda()
     g = torch.empty(1, dtype=torch.float64, device="cuda")
     l = torch.empty(P, dtype=torch.float64, device="cuda")
-    eqb.eqb_max_violation(lt, T, K, g, l, [int(x) for x in off])
+    m = torch.empty(1, dtype=torch.float64, device="cuda")
+    eqb.eqb_max_violation(lt, T, K, g, l, [int(x) for x in off], m)
     torch.cuda.synchronize()
     want_g, want_l = B.max_violation(load, off, K)
     assert same_f64(g.cpu().numpy(), [want_g])
     assert same_f64(l.cpu().numpy(), want_l)
+    assert same_f64(m.cpu().numpy(), [B.local_maxvio_mean(want_l)])
 
 
 def check_loop(got, want):
@@ -59,6 +61,7 @@ def check_loop(got, want):
         np.testing.assert_array_equal(a["load"], b["load"], err_msg=f"step {q}")
         assert same_f64([a["maxvio_global"]], [b["maxvio_global"]]), q
         assert same_f64(a["maxvio_local"], b["maxvio_local"]), q
+        assert same_f64([a["maxvio_local_mean"]], [b["maxvio_local_mean"]]), q
         np.testing.assert_array_equal(a["bhat"], b["bhat"], err_msg=f"step {q}")
         np.testing.assert_array_equal(a["b_next"].view(np.uint32), b["b_next"].view(np.uint32))
 
