@@ -67,6 +67,8 @@ typedef int32_t eqb_status;
 #define EQB_ERR_UNSUPPORTED  2   /* E outside the supported set, misaligned z */
 #define EQB_ERR_RANK         3   /* r < 1 or r > number of counted margins */
 #define EQB_ERR_HIP          4   /* the HIP runtime reported a launch error */
+#define EQB_ERR_SCRATCH      5   /* eqb_layer_noalloc: the layer needs more than
+                                    EQB_NOALLOC_SCRATCH_BYTES of working memory */
 
 #define EQB_NBINS            256
 #define EQB_MAX_PARTITIONS   256
@@ -286,6 +288,27 @@ eqb_status eqb_layer(const uint16_t* z, const float* b, int64_t T, int32_t E, in
                      int32_t* load, uint16_t* q_bf16, float* b_next, int32_t* hist_hi_sum,
                      int32_t* hist_lo_sum, int32_t* dev_status, void* workspace, size_t workspace_bytes,
                      void* const* marks, void* stream);
+
+/*
+ * eqb_layer for callers that cannot allocate device memory (code under HIP
+ * graph capture, tight serving loops, harnesses that forbid hipMalloc): the
+ * same layer, the same outputs and argument checks, but the working buffers
+ * live in a library-owned device array of EQB_NOALLOC_SCRATCH_BYTES per GPU
+ * (held until the process ends) instead of a caller workspace.  The call
+ * allocates nothing; the caller still passes every input and output.
+ *   Limit: eqb_layer_workspace_size(E, P) <= EQB_NOALLOC_SCRATCH_BYTES, i.e.
+ *   P * E <= 4096 (E = 256: up to 16 partitions); larger layers return
+ *   EQB_ERR_SCRATCH before anything is enqueued.
+ *   Every call on one GPU shares that GPU's array: the call clears the part
+ *   it uses (a fill kernel) before the layer runs, and calls whose work may
+ *   overlap on one GPU (other streams, other threads) race on it and give
+ *   wrong results.  Order them on one stream.
+ */
+#define EQB_NOALLOC_SCRATCH_BYTES ((size_t)(8u << 20) + (64u << 10))
+eqb_status eqb_layer_noalloc(const uint16_t* z, const float* b, int64_t T, int32_t E, int32_t K,
+                             const int64_t* part_off, int32_t P, int32_t* topk_idx, float* topk_score,
+                             float* tau, int32_t* load, uint16_t* q_bf16, float* b_next,
+                             int32_t* hist_hi_sum, int32_t* hist_lo_sum, int32_t* dev_status, void* stream);
 
 /*
  * Test control (host only, no HIP call): caps the number of blocks of the

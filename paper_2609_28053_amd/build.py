@@ -11,7 +11,8 @@ import sys
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
-SOURCES = [os.path.join(CSRC, f) for f in ("eqb_api.hip", "margin.hip", "select.hip", "balance.hip", "variants.hip")]
+SOURCES = [os.path.join(CSRC, f) for f in ("eqb_api.hip", "margin.hip", "select.hip", "balance.hip", "variants.hip",
+                                          "layer_noalloc.hip")]
 # The routing kernels are compiled on their own, without IEEE mode: their
 # float maxima and medians then need no NaN quieting, which lets the compiler
 # fold each DPP group maximum into one instruction and schedule around its

@@ -331,6 +331,7 @@ const char* eqb_status_string(eqb_status status) {
     case EQB_ERR_UNSUPPORTED: return "EQB_ERR_UNSUPPORTED";
     case EQB_ERR_RANK: return "EQB_ERR_RANK";
     case EQB_ERR_HIP: return "EQB_ERR_HIP";
+    case EQB_ERR_SCRATCH: return "EQB_ERR_SCRATCH";
     default: return "EQB_ERR_UNKNOWN";
   }
 }

@@ -24,6 +24,8 @@ EQB_ERR_INVALID_ARG = 1
 EQB_ERR_UNSUPPORTED = 2
 EQB_ERR_RANK = 3
 EQB_ERR_HIP = 4
+EQB_ERR_SCRATCH = 5
+EQB_NOALLOC_SCRATCH_BYTES = (8 << 20) + (64 << 10)
 EQB_NBINS = 256
 EQB_MAX_PARTITIONS = 256
 EQB_DEV_RANK_EXCEEDS_COUNT = 1
@@ -45,6 +47,7 @@ EXPORTS = (
     "eqb_lei_router_backward",
     "eqb_layer_workspace_size",
     "eqb_layer",
+    "eqb_layer_noalloc",
     "eqb_set_max_blocks",
     "eqb_get_max_blocks",
     "eqb_rank",
@@ -78,6 +81,7 @@ def _load():
         "eqb_lei_router_backward": [P, P, P, P, i64, i32, i32, P, i32, P, P],
         "eqb_layer_workspace_size": [i32, i32],
         "eqb_layer": [P, P, i64, i32, i32, P, i32, P, P, P, P, P, P, P, P, P, P, ctypes.c_size_t, P, P],
+        "eqb_layer_noalloc": [P, P, i64, i32, i32, P, i32, P, P, P, P, P, P, P, P, P, P],
         "eqb_set_max_blocks": [i32],
         "eqb_get_max_blocks": [],
         "eqb_rank": [i64, i32, i32],
@@ -340,6 +344,21 @@ def eqb_layer(z, b, K, topk_idx, topk_score, tau, load, q_bf16, b_next, dev_stat
         _ptr(hist_lo_sum, torch.int32, E * EQB_NBINS, "hist_lo_sum"),
         _ptr(dev_status, torch.int32, 1, "dev_status"), _ptr(workspace, torch.uint8, name="workspace"),
         workspace.numel(), marks, _stream(stream)))
+    del keep
+
+
+def eqb_layer_noalloc(z, b, K, topk_idx, topk_score, tau, load, q_bf16, b_next, dev_status, part_off=None,
+                      hist_hi_sum=None, hist_lo_sum=None, stream=None):
+    T, E = z.shape
+    po, P, keep = _offsets(part_off, T)
+    _check("eqb_layer_noalloc", lib.eqb_layer_noalloc(
+        _ptr(z, _Z, name="z"), _ptr(b, torch.float32, E, "b"), T, E, K, po, P,
+        _ptr(topk_idx, torch.int32, T * K, "topk_idx"), _ptr(topk_score, torch.float32, T * K, "topk_score"),
+        _ptr(tau, torch.float32, T, "tau"), _ptr(load, torch.int32, P * E, "load"),
+        _ptr(q_bf16, _Z, E, "q_bf16"), _ptr(b_next, torch.float32, E, "b_next"),
+        _ptr(hist_hi_sum, torch.int32, E * EQB_NBINS, "hist_hi_sum"),
+        _ptr(hist_lo_sum, torch.int32, E * EQB_NBINS, "hist_lo_sum"),
+        _ptr(dev_status, torch.int32, 1, "dev_status"), _stream(stream)))
     del keep
 
 

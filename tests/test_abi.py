@@ -241,3 +241,20 @@ def test_grid_cap_is_per_thread(lib):
         assert lib.eqb_set_max_blocks(0) == OK
     assert lib.eqb_set_max_blocks(-1) == INVALID
 
+
+
+def test_noalloc_layer_rejects_before_any_hip_call(lib):
+    """The scratch limit and the argument checks come before the library
+    touches the runtime (this container has no GPU)."""
+    f = lib.eqb_layer_noalloc
+    f.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32,
+                  ctypes.c_void_p, ctypes.c_int32] + [ctypes.c_void_p] * 10
+    SCRATCH = 5
+    po, keep = offs(*range(0, 18 * 64, 64)[:18])           # 17 partitions
+    assert f(FAKE, FAKE, 17 * 64 - 64, 256, 8, po, 17, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, None, FAKE,
+             None) == SCRATCH                               # 17 * 256 > 4096
+    assert lib.eqb_status_string(SCRATCH) == b"EQB_ERR_SCRATCH"
+    assert f(FAKE, FAKE, 64, 8, 8, None, 1, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, None, FAKE, None) == INVALID
+    assert f(FAKE, FAKE, 64, 12, 2, None, 1, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, None, FAKE, None) == UNSUPPORTED
+    assert f(FAKE, FAKE, 0, 8, 2, None, 1, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, None, FAKE, None) == RANK
+    assert f(FAKE, FAKE, 64, 8, 2, None, 1, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, None, None, None) == INVALID
