@@ -8,7 +8,7 @@ import pytest
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 HEADER = os.path.join(ROOT, "include", "eqb.h")
-LIB = os.path.join(ROOT, "paper_2609_28053_amd", "libeqb.so")
+LIB = os.environ.get("EQB_LIB", os.path.join(ROOT, "paper_2609_28053_amd", "libeqb.so"))
 
 OK, INVALID, UNSUPPORTED, RANK = 0, 1, 2, 3
 
