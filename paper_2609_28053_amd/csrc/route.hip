@@ -13,9 +13,11 @@
 // kList-1 medians per element).  Keys are compared as floats, so negative
 // scores order correctly; the key's sum takes -0 in b as +0, so a score of
 // -0 keys as +0 and the two zeros share one run of keys.
-// K+2 extraction rounds then take the group maximum of the list heads with
-// DPP and pop the winner (the generic-K variant refills a lane whose list
-// runs dry; the unrolled variants send such rows to the exact path).  Key order is
+// K+1 extraction rounds then take the group maximum of the list heads with
+// DPP and pop the winner; the largest head left is rank K+1.  A lane whose
+// list runs dry is refilled below its last key (generic-K variant) or, in
+// the unrolled variants, scanned once for its next key, and a row whose
+// rounds missed a key is extracted again with refilled lists.  Key order is
 // score order except between scores that agree in their top 24 bits;
 // extraction continues until the last key leaves the top-24-bit run of rank
 // K, the winners' exact scores are recomputed from z and b, and a row whose
@@ -29,7 +31,13 @@
 namespace eqb {
 
 constexpr int kRmax = 16;              // extracted ranks kept per row
-constexpr int kList = 6;               // sorted keys kept per lane
+// Sorted keys kept per lane.  With eight lanes per row (E >= 64) a lane
+// holds five or more of a row's top K+1 keys in about one wave in fourteen
+// of the large E = 256, K = 8 workload; such lanes are settled by one scan
+// for their next key (below), which costs less than a sixth list level in
+// every row.  Narrower rows (fewer lanes each holding a larger share of
+// the top keys) keep six.
+template <int E> constexpr int kListOf = E >= 64 ? 5 : 6;
 constexpr int kFastKmax = kRmax - 2;
 // Block of the fast kernel: 12 waves, three per SIMD, so that a wave may hold
 // up to 168 VGPRs (with 16 waves the cap of 128 forces spills).
@@ -138,6 +146,7 @@ __global__ __launch_bounds__(kRouteBlock) void route_fast_kernel(
   constexpr int RSLOT = (kRmax + G - 1) / G;
   static_assert(N % 4 == 0 && N >= 8, "layout");
   static_assert(KT == 0 || KT + 2 <= E, "K+2 keys must exist");
+  constexpr int kList = kListOf<E>;
   const int K = KT > 0 ? KT : Kdyn;
 
   __shared__ __align__(16) uint32_t sh_hist[fast_hist_words<E>()];
@@ -298,6 +307,7 @@ __global__ __launch_bounds__(kRouteBlock) void route_fast_kernel(
     if constexpr (KT > 0) {
       int mK = kKeyNone, prev = kKeyNone;
       bool near = false;      // two adjacent extracted keys share their top 24 bits
+      const int tail = L[kList - 1];   // the smallest key a lane can pop
 #pragma unroll
       for (int k = 0; k <= KT; ++k) {
         const int M = group_max_key<G>(L[0]);
@@ -308,13 +318,36 @@ __global__ __launch_bounds__(kRouteBlock) void route_fast_kernel(
         if (k == KT) mK = M;
       }
       // Rank K+1 is the largest list head left.  Whether it shares the top 24
-      // bits of rank K, and whether a list ran dry, are read off the heads
-      // directly; the rest of each list is not needed past this point (a row
-      // that extends its run rebuilds its lists), so the last rounds' pops
-      // only shift the entries that later rounds read.  A dry head (-inf)
-      // never matches: no finite key has the top 24 bits of -inf.
-      const int head = ((uint32_t)(L[0] ^ mK) < 256u) ? 1 : 0;
-      const int rowflag = group_max_i32<G>(L[0] == kKeyNone ? 2 : head);
+      // bits of rank K is read off the heads directly; the rest of each list
+      // is not needed past this point (a row that extends its run rebuilds
+      // its lists), so the last rounds' pops only shift the entries that
+      // later rounds read.
+      // A lane whose list ran dry popped all of its kList keys and has no
+      // head: its next key is the largest of its keys below the last one it
+      // popped, found by one scan of its logits.  If that key ranks above
+      // rank K, the rounds missed it and the row is extracted again; if not,
+      // it is the lane's head.  A head of -inf (no key left) never matches:
+      // no finite key has the top 24 bits of -inf.
+      int hk = L[0];
+      bool missed = false;
+      if (__builtin_expect(__any(L[0] == kKeyNone), 0)) {
+        const bool dry_lane = L[0] == kKeyNone;
+        int nxt = kKeyNone;
+#pragma unroll
+        for (int q = 0; q < NQ; ++q) {
+          const float4 bq = bias4(q);
+          const uint32_t ipk = idxpk(q);
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const int x = key_of(zf[q * 4 + i], pick(bq, i), ipk, i);
+            nxt = key_lt(x, tail) ? key_max(nxt, x) : nxt;
+          }
+        }
+        hk = dry_lane ? nxt : hk;
+        missed = dry_lane && key_lt(mK, nxt);
+      }
+      const int head = ((uint32_t)(hk ^ mK) < 256u) ? 1 : 0;
+      const int rowflag = group_max_i32<G>(missed ? 2 : head);
       // z of the experts at this lane's ranks, recovered from their keys.
       // Every slot's bias is read before any is used, so the LDS latency is
       // paid once; one wave-wide test sends the failed recoveries to memory.
@@ -358,11 +391,11 @@ __global__ __launch_bounds__(kRouteBlock) void route_fast_kernel(
         }
       }
       const int tauhi = mK >> 8;
-      const bool dry = rowflag == 2;
+      const bool dry = rowflag == 2;   // the rounds missed a key of a dry lane
       slow = valid && !bias_ok;
       staged = valid && !slow && (near || rowflag != 0);
       nrank = KT + 1;
-      if (__any(staged)) {
+      if (__builtin_expect(__any(staged), 0)) {
         // stage the keys, extend the run of rank K if it continues, then exact scores
 #pragma unroll
         for (int s = 0; s < RSLOT; ++s) {
@@ -393,10 +426,11 @@ __global__ __launch_bounds__(kRouteBlock) void route_fast_kernel(
           }
         }
         bad = bad || ext;           // the run is longer than the rank buffer
-        // Rows where a lane's list ran dry redo the extraction from fresh
-        // lists, refilling a lane's list below its last key whenever it runs
-        // dry again (as the generic-K loop does); only a run longer than the
-        // rank buffer still goes to the exact 64-bit path.
+        // Rows whose rounds missed a key (a lane held more of the top K+1
+        // keys than its list) redo the extraction from fresh lists, refilling
+        // a lane's list below its last key whenever it runs dry again (as the
+        // generic-K loop does); only a run longer than the rank buffer still
+        // goes to the exact 64-bit path.
         bool redo = staged && dry;
         if (__any(redo)) {
           if (redo) rebuild(zf, kKeyTop, L);
@@ -488,7 +522,7 @@ __global__ __launch_bounds__(kRouteBlock) void route_fast_kernel(
       const float fa = __uint_as_float(a.x), fc = __uint_as_float(c.x);
       return fa > fc || (fa == fc && (a.y & 0xFF) < (c.y & 0xFF));
     };
-    if (__any(staged)) {
+    if (__builtin_expect(__any(staged), 0)) {
       bool coll = false;
 #pragma unroll
       for (int s = 0; s < RSLOT; ++s) {
@@ -513,7 +547,7 @@ __global__ __launch_bounds__(kRouteBlock) void route_fast_kernel(
     }
 
     // ---- exact 64-bit extraction for rows flagged slow
-    if (__any(slow)) {
+    if (__builtin_expect(__any(slow), 0)) {
       if (slow) {
         uint64_t prevk = ~0ull;
         for (int k = 0; k <= K; ++k) {

@@ -131,10 +131,11 @@ def test_every_E_and_K_extremes(eqb, E):
 @pytest.mark.parametrize("E,K", [(64, 8), (64, 6), (128, 6), (256, 8), (256, 6)])
 def test_lists_run_dry(eqb, E, K):
     """Rows whose top ranks crowd into the experts of one lane.  The fast
-    route kernel keeps six keys per lane (lane g of a row holds the experts
-    with (e >> 2) % 8 == g); a lane holding more of the top K+1 keys runs
-    dry, and the row is extracted again with refilled lists.  Some rows also
-    carry exact ties, so dry rows meet the exact ordering of tied scores."""
+    route kernel keeps five keys per lane at E >= 64 (lane g of a row holds
+    the experts with (e >> 2) % 8 == g); a lane holding more of the top K+1
+    keys runs dry, and the row is extracted again with refilled lists.  Some
+    rows also carry exact ties, so dry rows meet the exact ordering of tied
+    scores."""
     rng = np.random.default_rng(1000 + E + K)
     T = 3001
     x = rng.standard_normal((T, E)).astype(np.float32)
@@ -150,6 +151,40 @@ def test_lists_run_dry(eqb, E, K):
     b[rng.integers(0, E, 5)] = np.float32(0.25)
     off = np.array([0, 1000, 2001, T], np.int64)
     say(f"dry lists E={E} K={K} T={T}")
+    assert_parity(gpu_layer(eqb, z, b, K, off), O.run_layer(z, b, K, off), K)
+
+
+@pytest.mark.parametrize("E,K", [(64, 6), (128, 8), (256, 8), (256, 6), (256, 7)])
+def test_dry_lane_next_key(eqb, E, K):
+    """A lane of the fast kernel (five keys per lane at E >= 64; lane g holds
+    the experts with (e >> 2) % 8 == g) that holds exactly five of the top
+    K+1 keys pops its whole list; its next key is then found by a scan.
+    Each row puts five experts of one lane on top and the rest of the top K+1
+    in other lanes, and places that lane's sixth expert (a) far below rank
+    K, (b) just below rank K, (c) on rank K's score (a tie that the lower
+    index breaks), (d) just above rank K (the rounds missed it and the row is
+    extracted again), or (e) two binary32 ulps below rank K's score, sharing
+    its top 24 bits (the run past rank K continues)."""
+    rng = np.random.default_rng(4100 + E + K)
+    T = 5 * 1200 + 7
+    lane = (np.arange(E) >> 2) % 8
+    x = (rng.standard_normal((T, E)) * 0.5 - 3.0).astype(np.float32)
+    # every expert outside lane 0 carries +2^-20: sums among them keep their
+    # ties, and a lane-0 expert on the same logit scores 2 ulps lower (the
+    # scores near rank K lie in [4, 8))
+    b = np.where(lane == 0, np.float32(0.0), np.float32(2.0 ** -20)).astype(np.float32)
+    rank_k = np.float32(6.0 - 0.5 * (K - 5))
+    for t in range(T):
+        c = t % 5
+        h = 0 if c == 4 else int(rng.integers(1, 8))
+        mine = rng.permutation(np.flatnonzero(lane == h))
+        other = rng.permutation(np.flatnonzero((lane != h) & (lane != 0)))
+        x[t, mine[:5]] = 8.0 + np.arange(5)[::-1]            # ranks 0..4, one lane
+        x[t, other[:K - 4]] = 6.0 - 0.5 * np.arange(K - 4)   # ranks 5..K, other lanes
+        x[t, mine[5]] = {0: -2.0, 1: rank_k - 0.25, 2: rank_k, 3: rank_k + 0.25, 4: rank_k}[c]
+    z = O.f32_to_bf16_rne(x.astype(np.float32))
+    off = np.array([0, T // 2, T], np.int64)
+    say(f"dry lane next key E={E} K={K} T={T}")
     assert_parity(gpu_layer(eqb, z, b, K, off), O.run_layer(z, b, K, off), K)
 
 
