@@ -207,7 +207,7 @@ __global__ __launch_bounds__(kRouteBlock) void route_fast_kernel(
   static_assert(fast_hist_words<E>() % 4 == 0, "16-byte zeroing");
   for (int w = threadIdx.x; w < fast_hist_words<E>() / 4; w += kRouteBlock)
     reinterpret_cast<uint4*>(sh_hist)[w] = make_uint4(0, 0, 0, 0);
-  int fits = 1;
+  int fits = 1, bzero = 1;
   for (int e = threadIdx.x; e < E; e += kRouteBlock) {
     sh_load[e] = 0;
     const float bv = b[e];
@@ -216,10 +216,17 @@ __global__ __launch_bounds__(kRouteBlock) void route_fast_kernel(
 #pragma unroll
     for (int c = 0; c < NQ; ++c) sh_bk[c][e ^ (c * 4 * G)] = bk;
     fits &= (int)(fabsf(bv) < 0x1p119f);
+    bzero &= (int)(bk == 0.0f);
   }
   // |z| <= 2^128 - 2^120 for a finite BF16 z, so with |b| < 2^119 every sum
   // z + b is finite and every key is a finite float.
   const bool bias_ok = __syncthreads_and(fits) != 0;
+  // With a zero bias (the starting point of the balancing loop) every score
+  // is a BF16 logit, so keys that agree in their top 24 bits hold equal
+  // scores (for scores of either sign the index byte then orders them by
+  // magnitude: lower index first for non-negative scores, last for negative
+  // ones).
+  const bool keys_exact = __syncthreads_and(bzero) != 0;
 
   uint2* myrank = sh_rank[wave][r];
 
@@ -256,7 +263,9 @@ __global__ __launch_bounds__(kRouteBlock) void route_fast_kernel(
   // t: row index inside the current segment
   // raw holds this step's logits (loaded one step earlier); once they are
   // widened, refill(raw) issues the next step's loads into the same registers.
-  auto process = [&](uint2 (&raw)[NQ], uint32_t t, bool valid, auto&& refill) __attribute__((always_inline)) {
+  // exact: std::true_type when the block's keys are exact (zero bias)
+  auto process = [&](auto exact, uint2 (&raw)[NQ], uint32_t t, bool valid, auto&& refill)
+                     __attribute__((always_inline)) {
     // ---- widen the logits once; build keys and the per-lane sorted list
     float4 bq = bias4(0);   // read first: its LDS latency passes during the widening
     float zf[N];
@@ -395,6 +404,13 @@ __global__ __launch_bounds__(kRouteBlock) void route_fast_kernel(
       slow = valid && !bias_ok;
       staged = valid && !slow && (near || rowflag != 0);
       nrank = KT + 1;
+      // A row is staged when adjacent ranks' keys agree in their top 24 bits
+      // (their order may be wrong) or the run of rank K's top 24 bits
+      // continues past it.  With exact keys such keys hold equal scores, and
+      // for a non-negative rank K (every rank at or above it non-negative)
+      // the index byte already orders them as the exact order does: only a
+      // missed key needs the staged path.
+      if constexpr (decltype(exact)::value) staged = staged && (dry || mK < 0);
       if (__builtin_expect(__any(staged), 0)) {
         // stage the keys, extend the run of rank K if it continues, then exact scores
 #pragma unroll
@@ -646,6 +662,9 @@ __global__ __launch_bounds__(kRouteBlock) void route_fast_kernel(
     __builtin_amdgcn_wave_barrier();
   };
 
+  // The sweep is compiled twice, for exact keys (a zero bias) and for any
+  // bias, so that neither carries the other's test in its per-row path.
+  auto sweep = [&](auto exact) __attribute__((always_inline)) {
   bool first = true;
   for_each_segment(r0, r1, pt, [&](int p, int64_t s0, int64_t s1) {
     const int64_t su = wave_uniform(s0);
@@ -665,7 +684,7 @@ __global__ __launch_bounds__(kRouteBlock) void route_fast_kernel(
     first = false;
     for (uint32_t base = 0; base < n; base += ROWS) {
       const uint32_t t = base + wave * R + r;
-      process(buf, t, t < n, [&](uint2 (&dst)[NQ]) { load_step(dst, seg_z, base + ROWS, n); });
+      process(exact, buf, t, t < n, [&](uint2 (&dst)[NQ]) { load_step(dst, seg_z, base + ROWS, n); });
     }
     __syncthreads();
     if (hist) {
@@ -681,6 +700,9 @@ __global__ __launch_bounds__(kRouteBlock) void route_fast_kernel(
     }
     __syncthreads();
   });
+  };
+  if (keys_exact) sweep(std::true_type{});
+  else sweep(std::false_type{});
 }
 
 // ----------------------------------------------------------- generic ----
