@@ -17,11 +17,24 @@ constexpr int kWaves = kBlock / 64;
 constexpr int64_t kSegMax = 65535;      // rows per LDS histogram flush (16-bit counters)
 constexpr int kHistStride = kNBins + 1; // LDS words per expert pair (odd stride spreads banks)
 
-// Contiguous token partitions [off[p], off[p+1]), passed by value.
+// Contiguous token partitions [off[p], off[p+1]), passed by value.  nsub:
+// count slabs per partition (1 for the entry points that write a caller's
+// [P,E,256] counts; the one-call layer spreads a partition's blocks over
+// several slabs of its workspace, summed by the selections).
 struct PartTable {
   int64_t off[EQB_MAX_PARTITIONS + 1];
   int32_t P;
+  int32_t nsub = 1;
 };
+
+// The [E,256] count slab that this block adds partition p's counts to: with
+// nsub slabs per partition, block b uses slab b % nsub, so that fewer blocks
+// add to each counter (the flushes' global atomics on one address
+// serialise).
+__device__ __forceinline__ int32_t* count_slab(int32_t* hist, const PartTable& pt, int p, int E) {
+  const int sub = pt.nsub > 1 ? (int)(blockIdx.x % (unsigned)pt.nsub) : 0;
+  return hist + ((int64_t)p * pt.nsub + sub) * E * kNBins;
+}
 
 // ------------------------------------------------------------ BF16 ------
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }

@@ -37,7 +37,7 @@ eqb_status launch_select(int pass, const int32_t* hist, int P, int E, int64_t r,
                          int64_t* rank_in_bin, int32_t* sel_lo, uint16_t* q_bf16, float* b_next,
                          int32_t* hist_sum, int32_t* status, hipStream_t s);
 
-eqb_status launch_layer_selects(int pass, int32_t* hist, int P, int E, int64_t r, int32_t* sel_hi,
+eqb_status launch_layer_selects(int pass, int32_t* hist, int P, int nsub, int E, int64_t r, int32_t* sel_hi,
                                 int64_t* rank_in_bin, int32_t* sel_lo, uint16_t* q_bf16, float* b_next,
                                 int32_t* hist_sum, int32_t* load_acc, int32_t* load_out, int32_t* status,
                                 hipStream_t s);
@@ -61,14 +61,21 @@ eqb_status launch_lei_router_backward(const uint16_t* z, const int32_t* idx, con
 eqb_status launch_lei_inject(float* grad, const float* inj, int64_t T, int E, const PartTable& pt,
                              hipStream_t s);
 
+// Count slabs per partition in a layer's workspace: enough that about 16
+// slabs share the blocks of a launch (a partition of the large workload's
+// 16 already has its own), so no counter receives the flush atomics of
+// every block.
+inline int layer_replicas(int P) { return P >= 16 ? 1 : 16 / P; }
+
 // Working buffers of one layer (eqb_layer): the per-partition coarse and
-// fine counts, the loads as the route kernel accumulates them, and the
-// selections.  Each piece starts on a 256-byte boundary.  The counters are
-// zero when a layer starts and zero again when it ends: the selection that
-// reads a counter clears it.
+// fine counts (layer_replicas(P) slabs per partition), the loads as the
+// route kernel accumulates them, and the selections.  Each piece starts on a
+// 256-byte boundary.  The counters are zero when a layer starts and zero
+// again when it ends: the selection that reads a counter clears it.
 struct LayerWorkspace {
-  int32_t* hist_hi;       // [P,E,256]
-  int32_t* hist_lo;       // [P,E,256]
+  int nsub;               // count slabs per partition
+  int32_t* hist_hi;       // [P,nsub,E,256]
+  int32_t* hist_lo;       // [P,nsub,E,256]
   int32_t* load_acc;      // [P,E]
   int32_t* sel_hi;        // [E]
   int32_t* sel_lo;        // [E]
@@ -80,12 +87,14 @@ inline size_t align256(size_t n) { return (n + 255) & ~(size_t)255; }
 // Bytes of a layer workspace, and its pieces carved from base (null base:
 // only the size is computed).
 inline size_t layer_workspace(void* base, int E, int P, LayerWorkspace* w) {
-  const size_t hist = align256((size_t)P * E * kNBins * sizeof(int32_t));
+  const int nsub = layer_replicas(P);
+  const size_t hist = align256((size_t)P * nsub * E * kNBins * sizeof(int32_t));
   const size_t load = align256((size_t)P * E * sizeof(int32_t));
   const size_t sel = align256((size_t)E * sizeof(int32_t));
   const size_t rib = align256((size_t)E * sizeof(int64_t));
   if (base && w) {
     char* p = static_cast<char*>(base);
+    w->nsub = nsub;
     w->hist_hi = reinterpret_cast<int32_t*>(p);
     w->hist_lo = reinterpret_cast<int32_t*>(p + hist);
     w->load_acc = reinterpret_cast<int32_t*>(p + 2 * hist);

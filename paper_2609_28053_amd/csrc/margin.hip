@@ -125,7 +125,7 @@ __global__ __launch_bounds__(kBlock) void margin_hist_kernel(
       }
     }
     __syncthreads();
-    int32_t* slab = hist + (int64_t)p * E * kNBins;
+    int32_t* slab = count_slab(hist, pt, p, E);
     if (!kFine) {
       flush_hist<E, false>(sh_hist, slab, nullptr);
     } else {

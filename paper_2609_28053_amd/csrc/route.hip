@@ -688,8 +688,8 @@ __global__ __launch_bounds__(kRouteBlock) void route_fast_kernel(
     }
     __syncthreads();
     if (hist) {
-      if constexpr (kSlotHist<E>) flush_hist_slots<E>(sh_hist, hist + (int64_t)p * E * kNBins);
-      else flush_hist<E, false>(sh_hist, hist + (int64_t)p * E * kNBins, nullptr);
+      if constexpr (kSlotHist<E>) flush_hist_slots<E>(sh_hist, count_slab(hist, pt, p, E));
+      else flush_hist<E, false>(sh_hist, count_slab(hist, pt, p, E), nullptr);
     }
     if (load) {
       for (int e = threadIdx.x; e < E; e += kRouteBlock) {
@@ -771,7 +771,7 @@ __global__ __launch_bounds__(kBlock) void route_generic_kernel(
       }
     }
     __syncthreads();
-    if (hist) flush_hist<E, false>(sh_hist, hist + (int64_t)p * E * kNBins, nullptr);
+    if (hist) flush_hist<E, false>(sh_hist, count_slab(hist, pt, p, E), nullptr);
     if (load) {
       for (int e = threadIdx.x; e < E; e += kBlock) {
         const uint32_t c = sh_load[e];

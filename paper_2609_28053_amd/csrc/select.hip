@@ -43,7 +43,7 @@ __global__ __launch_bounds__(kNBins) void select_coarse_kernel(
     if (hist_sum) hist_sum[(int64_t)e * kNBins + u] = (int32_t)c;
     if (clear) slab_clear(hist + (int64_t)e * kNBins + u, P, (int64_t)E * kNBins);
     if (load_acc) {
-      for (int q = u; q < P; q += kNBins) {
+      for (int q = u; q < pt.P; q += kNBins) {
         load_out[(int64_t)q * E + e] = load_acc[(int64_t)q * E + e];
         load_acc[(int64_t)q * E + e] = 0;
       }
@@ -136,18 +136,21 @@ __global__ __launch_bounds__(256) void center_kernel(const uint16_t* __restrict_
   for (int e = threadIdx.x; e < E; e += blockDim.x) b_next[e] = (float)(val[e] - mean);
 }
 
-eqb_status launch_layer_selects(int pass, int32_t* hist, int P, int E, int64_t r, int32_t* sel_hi,
+// The layer's selections: the counts sit in P * nsub slabs, all summed; the
+// loads in P rows.
+eqb_status launch_layer_selects(int pass, int32_t* hist, int P, int nsub, int E, int64_t r, int32_t* sel_hi,
                                 int64_t* rank_in_bin, int32_t* sel_lo, uint16_t* q_bf16, float* b_next,
                                 int32_t* hist_sum, int32_t* load_acc, int32_t* load_out, int32_t* status,
                                 hipStream_t s) {
   PartTable none{};
   none.P = P;
+  const int nslabs = P * nsub;
   if (pass == 1) {
-    select_coarse_kernel<false><<<E, kNBins, 0, s>>>(hist, P, E, 0, r, none, sel_hi, rank_in_bin, hist_sum,
+    select_coarse_kernel<false><<<E, kNBins, 0, s>>>(hist, nslabs, E, 0, r, none, sel_hi, rank_in_bin, hist_sum,
                                                      nullptr, true, load_acc, load_out);
     return launch_status();
   }
-  select_fine_kernel<false><<<E, kNBins, 0, s>>>(hist, P, E, none, sel_hi, rank_in_bin, sel_lo, q_bf16,
+  select_fine_kernel<false><<<E, kNBins, 0, s>>>(hist, nslabs, E, none, sel_hi, rank_in_bin, sel_lo, q_bf16,
                                                  hist_sum, nullptr, true);
   if (launch_status() != EQB_OK) return EQB_ERR_HIP;
   center_kernel<<<1, 256, 0, s>>>(q_bf16, E, b_next, sel_lo, status, sel_hi, rank_in_bin);
@@ -165,13 +168,14 @@ eqb_status launch_layer(const RouteArgs& route, int64_t r, const LayerWorkspace&
   RouteArgs a = route;
   a.load = w.load_acc;
   a.hist = w.hist_hi;
+  a.pt.nsub = w.nsub;
   eqb_status st = mark(marks, 0, s);
   if (st != EQB_OK) return st;
   st = launch_route(a, s);
   if (st != EQB_OK) return st;
   if ((st = mark(marks, 1, s)) != EQB_OK) return st;
   const int P = a.pt.P, E = a.E;
-  st = launch_layer_selects(1, w.hist_hi, P, E, r, w.sel_hi, w.rank_in_bin, nullptr, nullptr, nullptr,
+  st = launch_layer_selects(1, w.hist_hi, P, w.nsub, E, r, w.sel_hi, w.rank_in_bin, nullptr, nullptr, nullptr,
                             hist_hi_sum, w.load_acc, load_out, nullptr, s);
   if (st != EQB_OK) return st;
   if ((st = mark(marks, 2, s)) != EQB_OK) return st;
@@ -186,7 +190,7 @@ eqb_status launch_layer(const RouteArgs& route, int64_t r, const LayerWorkspace&
   st = launch_margin(true, m, s);
   if (st != EQB_OK) return st;
   if ((st = mark(marks, 3, s)) != EQB_OK) return st;
-  st = launch_layer_selects(2, w.hist_lo, P, E, r, w.sel_hi, w.rank_in_bin, w.sel_lo, q_bf16, b_next,
+  st = launch_layer_selects(2, w.hist_lo, P, w.nsub, E, r, w.sel_hi, w.rank_in_bin, w.sel_lo, q_bf16, b_next,
                             hist_lo_sum, nullptr, nullptr, dev_status, s);
   if (st != EQB_OK) return st;
   return mark(marks, 4, s);

@@ -196,10 +196,13 @@ def layer(lib, T=64, E=8, K=2, ws=ctypes.c_void_p(0x10000), ws_bytes=1 << 30, po
 
 
 def test_layer_workspace_size(lib):
-    # two [P,E,256] int32 count slabs, the [P,E] loads and three [E] selections,
-    # each rounded up to 256 bytes
-    for E, P in ((8, 1), (64, 4), (256, 16), (256, 256)):
-        want = 2 * P * E * 1024 + -(-4 * P * E // 256) * 256 + 2 * -(-4 * E // 256) * 256 + -(-8 * E // 256) * 256
+    # two sets of [P,nsub,E,256] int32 count slabs (nsub = 16 // P slabs per
+    # partition below 16 partitions, else 1), the [P,E] loads and three [E]
+    # selections, each rounded up to 256 bytes
+    for E, P in ((8, 1), (64, 4), (128, 3), (256, 1), (256, 16), (256, 17), (256, 256)):
+        nsub = 1 if P >= 16 else 16 // P
+        want = (2 * P * nsub * E * 1024 + -(-4 * P * E // 256) * 256 + 2 * -(-4 * E // 256) * 256
+                + -(-8 * E // 256) * 256)
         assert lib.eqb_layer_workspace_size(E, P) == want
     assert lib.eqb_layer_workspace_size(12, 1) == 0
     assert lib.eqb_layer_workspace_size(8, 0) == 0
@@ -215,7 +218,7 @@ def test_layer_argument_checks(lib):
     assert layer(lib, ws_bytes=lib.eqb_layer_workspace_size(8, 1) - 1) == INVALID
     assert layer(lib, z=ctypes.c_void_p(0x10002)) == UNSUPPORTED
     po, keep = offs(0, 10, 64)
-    assert layer(lib, po=po, P=2, ws_bytes=lib.eqb_layer_workspace_size(8, 1)) == INVALID   # sized for P=1
+    assert layer(lib, po=po, P=2, ws_bytes=lib.eqb_layer_workspace_size(8, 2) - 1) == INVALID   # one byte short
     bad, keep2 = offs(0, 70, 64)
     assert layer(lib, po=bad, P=2) == INVALID
 
