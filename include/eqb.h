@@ -304,7 +304,7 @@ eqb_status eqb_layer(const uint16_t* z, const float* b, int64_t T, int32_t E, in
  *   overlap on one GPU (other streams, other threads) race on it and give
  *   wrong results.  Order them on one stream.
  */
-#define EQB_NOALLOC_SCRATCH_BYTES ((size_t)(8u << 20) + (64u << 10))
+#define EQB_NOALLOC_SCRATCH_BYTES ((size_t)(8u << 20) + (192u << 10))
 eqb_status eqb_layer_noalloc(const uint16_t* z, const float* b, int64_t T, int32_t E, int32_t K,
                              const int64_t* part_off, int32_t P, int32_t* topk_idx, float* topk_score,
                              float* tau, int32_t* load, uint16_t* q_bf16, float* b_next,

@@ -25,6 +25,9 @@ struct PartTable {
   int64_t off[EQB_MAX_PARTITIONS + 1];
   int32_t P;
   int32_t nsub = 1;
+  // Claim counters of the partitions' dynamic tails (one int32 per
+  // partition, 256 bytes apart, zero at launch), or null: see block_plan.
+  int32_t* pool = nullptr;
 };
 
 // The [E,256] count slab that this block adds partition p's counts to: with
@@ -267,13 +270,14 @@ __device__ __forceinline__ void slab_clear(int32_t* __restrict__ hist, int P, in
 // Calls f(p, s0, s1) for every piece of [r0, r1) lying in one partition and
 // holding at most kSegMax rows.  Uniform across the block.
 template <class F>
-__device__ __forceinline__ void for_each_segment(int64_t r0, int64_t r1, const PartTable& pt, F&& f) {
+__device__ __forceinline__ void for_each_segment(int64_t r0, int64_t r1, const PartTable& pt, F&& f,
+                                                 int64_t seg_max = kSegMax) {
   int p = 0;
   int64_t t = r0;
   while (t < r1) {
     while (p < pt.P - 1 && pt.off[p + 1] <= t) ++p;
     int64_t end = pt.off[p + 1] < r1 ? pt.off[p + 1] : r1;
-    if (end - t > kSegMax) end = t + kSegMax;
+    if (end - t > seg_max) end = t + seg_max;
     f(p, t, end);
     t = end;
   }
@@ -281,13 +285,14 @@ __device__ __forceinline__ void for_each_segment(int64_t r0, int64_t r1, const P
 
 // The same pieces in reverse order (last rows first).
 template <class F>
-__device__ __forceinline__ void for_each_segment_rev(int64_t r0, int64_t r1, const PartTable& pt, F&& f) {
+__device__ __forceinline__ void for_each_segment_rev(int64_t r0, int64_t r1, const PartTable& pt, F&& f,
+                                                     int64_t seg_max = kSegMax) {
   int p = pt.P - 1;
   int64_t t = r1;
   while (t > r0) {
     while (p > 0 && pt.off[p] >= t) --p;
     int64_t start = pt.off[p] > r0 ? pt.off[p] : r0;
-    if (t - start > kSegMax) start = t - kSegMax;
+    if (t - start > seg_max) start = t - seg_max;
     f(p, start, t);
     t = start;
   }
@@ -392,6 +397,72 @@ __device__ __forceinline__ int64_t wave_uniform(int64_t x) {
 __device__ __forceinline__ void block_rows(int64_t T, int64_t rows_per_block, int64_t* r0, int64_t* r1) {
   *r0 = (int64_t)blockIdx.x * rows_per_block;
   *r1 = (*r0 + rows_per_block < T) ? *r0 + rows_per_block : T;
+}
+
+// Dynamic tails (the one-call layer's route sweep).  Compute units do not
+// sweep at one speed (the blocks of a launch finish up to ~5% apart), so a
+// static split waits for the slowest.  With pt.pool set, the blocks of a
+// launch are dealt out to the partitions in proportion to their rows (block
+// b serves partition p when floor(nb off[p] / T) <= b < floor(nb off[p+1] /
+// T); the host checks that every non-empty partition gets a block), and a
+// partition's blocks form groups of at most kGroupBlocks, each taking a share
+// of the partition's rows in proportion to its blocks.  A group keeps the
+// last 1/kPoolDiv of its rows (at most kPoolMax) as a pool and splits the rest
+// into contiguous static ranges, one per block; once a wave has finished its
+// block's range it claims pool chunks from the group's counter until none is
+// left.  Groups keep the claims on one counter few.  Static ranges are
+// flushed every kSegPool rows, so a block's last static segment plus any pool
+// rows it takes stay below the 16-bit LDS counters' limit.
+constexpr int64_t kPoolMax = 16384;
+constexpr int64_t kPoolDiv = 12;
+constexpr int kGroupBlocks = 16;
+constexpr int64_t kSegPool = kSegMax - kPoolMax;
+// A group's claim counter is indexed by the group's first block and sits on
+// its own 128-byte line; pool mode is used for grids of at most
+// kPoolCounters blocks.
+constexpr int kPoolStride = 32;
+constexpr int kPoolCounters = 1024;
+
+struct BlockPlan {
+  int64_t r0, r1;     // the block's static rows
+  int64_t q0, q1;     // its group's pool (pool mode)
+  int p;              // the partition served (pool mode), else -1
+  int ctr;            // its group's counter (pool mode)
+  bool pool;
+};
+
+inline __host__ __device__ int64_t pool_block_start(const PartTable& pt, int64_t T, int64_t nb, int p) {
+  return nb * pt.off[p] / T;
+}
+
+__device__ __forceinline__ BlockPlan block_plan(const PartTable& pt, int64_t T, int64_t rows_per_block) {
+  BlockPlan w;
+  w.p = -1;
+  w.ctr = 0;
+  w.q0 = w.q1 = 0;
+  w.pool = pt.pool != nullptr;
+  if (!w.pool) {
+    block_rows(T, rows_per_block, &w.r0, &w.r1);
+    return w;
+  }
+  const int64_t nb = gridDim.x, b = blockIdx.x;
+  // block b serves p when nb off[p] < (b + 1) T <= nb off[p+1]
+  int p = 0;
+  while (p < pt.P - 1 && nb * pt.off[p + 1] < (b + 1) * T) ++p;
+  const int64_t b0 = pool_block_start(pt, T, nb, p), m = pool_block_start(pt, T, nb, p + 1) - b0;
+  const int64_t n = pt.off[p + 1] - pt.off[p], i = b - b0;
+  const int64_t gb0 = (i / kGroupBlocks) * kGroupBlocks;
+  const int64_t gb1 = gb0 + kGroupBlocks < m ? gb0 + kGroupBlocks : m;
+  const int64_t g0 = pt.off[p] + n * gb0 / m, g1 = pt.off[p] + n * gb1 / m;   // the group's rows
+  const int64_t gn = g1 - g0, q = gn / kPoolDiv < kPoolMax ? gn / kPoolDiv : kPoolMax;
+  const int64_t s = gn - q, j = i - gb0, mg = gb1 - gb0;
+  w.p = p;
+  w.ctr = (int)(b0 + gb0);
+  w.r0 = g0 + s * j / mg;
+  w.r1 = g0 + s * (j + 1) / mg;
+  w.q0 = g0 + s;
+  w.q1 = g1;
+  return w;
 }
 
 }  // namespace eqb

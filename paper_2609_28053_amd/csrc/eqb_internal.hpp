@@ -40,7 +40,7 @@ eqb_status launch_select(int pass, const int32_t* hist, int P, int E, int64_t r,
 eqb_status launch_layer_selects(int pass, int32_t* hist, int P, int nsub, int E, int64_t r, int32_t* sel_hi,
                                 int64_t* rank_in_bin, int32_t* sel_lo, uint16_t* q_bf16, float* b_next,
                                 int32_t* hist_sum, int32_t* load_acc, int32_t* load_out, int32_t* status,
-                                hipStream_t s);
+                                int32_t* pool_reset, hipStream_t s);
 
 eqb_status launch_select_local(int pass, const int32_t* hist, int E, int K, const PartTable& pt,
                                int32_t* sel_hi, int64_t* rank_in_bin, int32_t* sel_lo, uint16_t* q_bf16,
@@ -80,6 +80,7 @@ struct LayerWorkspace {
   int32_t* sel_hi;        // [E]
   int32_t* sel_lo;        // [E]
   int64_t* rank_in_bin;   // [E]
+  int32_t* pool;          // claim counters of the route sweep's dynamic tails (kPoolCounters, kPoolStride apart)
 };
 
 inline size_t align256(size_t n) { return (n + 255) & ~(size_t)255; }
@@ -92,6 +93,7 @@ inline size_t layer_workspace(void* base, int E, int P, LayerWorkspace* w) {
   const size_t load = align256((size_t)P * E * sizeof(int32_t));
   const size_t sel = align256((size_t)E * sizeof(int32_t));
   const size_t rib = align256((size_t)E * sizeof(int64_t));
+  const size_t pool = (size_t)kPoolCounters * kPoolStride * sizeof(int32_t);
   if (base && w) {
     char* p = static_cast<char*>(base);
     w->nsub = nsub;
@@ -101,8 +103,9 @@ inline size_t layer_workspace(void* base, int E, int P, LayerWorkspace* w) {
     w->sel_hi = reinterpret_cast<int32_t*>(p + 2 * hist + load);
     w->sel_lo = reinterpret_cast<int32_t*>(p + 2 * hist + load + sel);
     w->rank_in_bin = reinterpret_cast<int64_t*>(p + 2 * hist + load + 2 * sel);
+    w->pool = reinterpret_cast<int32_t*>(p + 2 * hist + load + 2 * sel + rib);
   }
-  return 2 * hist + load + 2 * sel + rib;
+  return 2 * hist + load + 2 * sel + rib + pool;
 }
 
 // The whole layer on one stream: route + loads + coarse counts, coarse
@@ -146,5 +149,27 @@ inline void grid_for(int64_t T, int rows_per_step, int blocks_per_cu, int* block
 }
 
 inline eqb_status launch_status() { return hipGetLastError() == hipSuccess ? EQB_OK : EQB_ERR_HIP; }
+
+// The partition table for a launch of `blocks` blocks: pool mode (pt.pool)
+// is kept only when every non-empty partition gets a block of its own under
+// block_plan's proportional deal and a block's share is at least min_rows
+// (small batches gain nothing from it), else the table falls back to static
+// ranges.
+inline PartTable pool_table(const PartTable& pt, int64_t T, int blocks, int64_t min_rows) {
+  PartTable out = pt;
+  if (out.pool == nullptr) return out;
+  if (blocks > kPoolCounters || T < min_rows * blocks) {
+    out.pool = nullptr;
+    return out;
+  }
+  for (int p = 0; p < pt.P; ++p) {
+    if (pt.off[p + 1] > pt.off[p] &&
+        pool_block_start(pt, T, blocks, p + 1) <= pool_block_start(pt, T, blocks, p)) {
+      out.pool = nullptr;
+      break;
+    }
+  }
+  return out;
+}
 
 }  // namespace eqb

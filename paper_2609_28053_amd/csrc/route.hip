@@ -158,6 +158,7 @@ __global__ __launch_bounds__(kRouteBlock) void route_fast_kernel(
   // the 64 banks) would put every row's reads on the same 32 banks.
   __shared__ float sh_bk[NQ][E + kBiasPad];
   __shared__ uint2 sh_rank[kRouteWaves][R][kRmax];   // (score bits, zbits << 16 | e) in rank order
+  __shared__ int sh_pool_spent;                       // the group's pool has run out (pool mode)
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int g = lane % G, r = lane / G;
@@ -182,25 +183,29 @@ __global__ __launch_bounds__(kRouteBlock) void route_fast_kernel(
   // row instead (processed as invalid: no output, no count).  Byte offsets
   // stay below 2^25; the piece index occupies bits that the row and lane
   // parts leave clear, so XOR selects piece q ^ rr.
-  auto load_step = [&](uint2 (&dst)[NQ], const uint16_t* zb, uint32_t base, uint32_t n) {
-    uint32_t t = base + wave * R + r;
+  auto load_rows = [&](uint2 (&dst)[NQ], const uint16_t* zb, uint32_t wbase, uint32_t n) {
+    uint32_t t = wbase + r;
     t = t < n ? t : n - 1;
     const uint32_t off = (t * (uint32_t)E + (uint32_t)g * 4u) * 2u + (uint32_t)rr * (8u * G);
 #pragma unroll
     for (int q = 0; q < NQ; ++q) dst[q] = at<uint2>(zb, off ^ ((uint32_t)q * (8u * G)));
   };
+  auto load_step = [&](uint2 (&dst)[NQ], const uint16_t* zb, uint32_t base, uint32_t n) {
+    load_rows(dst, zb, base + wave * R, n);
+  };
 
   // The first step of the block's first segment (as for_each_segment will
   // cut it) is loaded before the LDS set-up, so that its latency passes while
   // the histogram is zeroed and the bias is staged.
-  int64_t r0, r1;
-  block_rows(T, rows_per_block, &r0, &r1);
+  const BlockPlan plan = block_plan(pt, T, rows_per_block);
+  const int64_t r0 = plan.r0, r1 = plan.r1;
+  const int64_t seg_max = plan.pool ? kSegPool : kSegMax;
   uint2 buf[NQ];
   if (r0 < r1) {
     int p = 0;
     while (p < pt.P - 1 && pt.off[p + 1] <= r0) ++p;
     int64_t end = pt.off[p + 1] < r1 ? pt.off[p + 1] : r1;
-    if (end - r0 > kSegMax) end = r0 + kSegMax;
+    if (end - r0 > seg_max) end = r0 + seg_max;
     load_step(buf, z + wave_uniform(r0) * E, 0, (uint32_t)(end - r0));
   }
 
@@ -208,6 +213,7 @@ __global__ __launch_bounds__(kRouteBlock) void route_fast_kernel(
   for (int w = threadIdx.x; w < fast_hist_words<E>() / 4; w += kRouteBlock)
     reinterpret_cast<uint4*>(sh_hist)[w] = make_uint4(0, 0, 0, 0);
   int fits = 1, bzero = 1;
+  if (threadIdx.x == 0) sh_pool_spent = 0;
   for (int e = threadIdx.x; e < E; e += kRouteBlock) {
     sh_load[e] = 0;
     const float bv = b[e];
@@ -664,14 +670,34 @@ __global__ __launch_bounds__(kRouteBlock) void route_fast_kernel(
 
   // The sweep is compiled twice, for exact keys (a zero bias) and for any
   // bias, so that neither carries the other's test in its per-row path.
-  auto sweep = [&](auto exact) __attribute__((always_inline)) {
-  bool first = true;
-  for_each_segment(r0, r1, pt, [&](int p, int64_t s0, int64_t s1) {
+  auto set_base = [&](int64_t s0) {
     const int64_t su = wave_uniform(s0);
     seg_z = z + su * E;
     seg_idx = topk_idx + su * K;
     seg_score = topk_score + su * K;
     seg_tau = tau + su;
+  };
+  // Adds the block's LDS counts (coarse bins, loads) of partition p to global
+  // memory and clears them.
+  auto flush_counts = [&](int p) {
+    __syncthreads();
+    if (hist) {
+      if constexpr (kSlotHist<E>) flush_hist_slots<E>(sh_hist, count_slab(hist, pt, p, E));
+      else flush_hist<E, false>(sh_hist, count_slab(hist, pt, p, E), nullptr);
+    }
+    if (load) {
+      for (int e = threadIdx.x; e < E; e += kRouteBlock) {
+        const uint32_t c = sh_load[e];
+        if (c) atomicAdd(&load[(int64_t)p * E + e], (int32_t)c);
+        sh_load[e] = 0;
+      }
+    }
+    __syncthreads();
+  };
+  auto sweep = [&](auto exact) __attribute__((always_inline)) {
+  bool first = true;
+  for_each_segment(r0, r1, pt, [&](int p, int64_t s0, int64_t s1) {
+    set_base(s0);
     const uint32_t n = (uint32_t)(s1 - s0);
     // The next step's loads are in flight while a step is processed: a step
     // widens the rows loaded one step earlier and then reuses their registers
@@ -686,20 +712,57 @@ __global__ __launch_bounds__(kRouteBlock) void route_fast_kernel(
       const uint32_t t = base + wave * R + r;
       process(exact, buf, t, t < n, [&](uint2 (&dst)[NQ]) { load_step(dst, seg_z, base + ROWS, n); });
     }
-    __syncthreads();
-    if (hist) {
-      if constexpr (kSlotHist<E>) flush_hist_slots<E>(sh_hist, count_slab(hist, pt, p, E));
-      else flush_hist<E, false>(sh_hist, count_slab(hist, pt, p, E), nullptr);
+    // in pool mode the last static segment's counts are flushed with the pool's
+    if (!(plan.pool && s1 == r1)) flush_counts(p);
+  }, seg_max);
+  if (plan.pool) {
+    // The group's pool, claimed by single waves in chunks of kChunk rows
+    // (kChunkSteps wave steps).  A wave claims its next chunk when it starts
+    // one and reads the claim at the start of the chunk's last step, whose
+    // refill loads the next chunk's first rows; that read waits only for
+    // loads the step waits for anyway.  A wave that draws past the pool
+    // marks it spent in LDS, and the block's other waves then stop claiming.
+    constexpr uint32_t kChunkSteps = 16;
+    constexpr uint32_t kChunk = (uint32_t)R * kChunkSteps;
+    set_base(plan.q0);
+    const uint32_t nq = (uint32_t)(plan.q1 - plan.q0);
+    const uint32_t nchunks = (nq + kChunk - 1) / kChunk;
+    int32_t* ctr = pt.pool + (int64_t)plan.ctr * kPoolStride;
+    volatile int* spent = &sh_pool_spent;
+    auto claim = [&]() -> uint32_t {
+      uint32_t v = nchunks;
+      if (lane == 0 && *spent == 0) v = (uint32_t)atomicAdd(ctr, 1);
+      return v;
+    };
+    auto take = [&](uint32_t v) -> uint32_t {
+      const uint32_t c = __builtin_amdgcn_readfirstlane(v);
+      if (c >= nchunks && lane == 0) *spent = 1;
+      return c;
+    };
+    uint32_t c = take(claim());
+    uint32_t pend = nchunks;
+    if (c < nchunks) {
+      load_rows(buf, seg_z, c * kChunk, nq);
+      pend = claim();
     }
-    if (load) {
-      for (int e = threadIdx.x; e < E; e += kRouteBlock) {
-        const uint32_t c = sh_load[e];
-        if (c) atomicAdd(&load[(int64_t)p * E + e], (int32_t)c);
-        sh_load[e] = 0;
+    while (c < nchunks) {
+      uint32_t cn = nchunks;
+#pragma unroll 1
+      for (uint32_t j = 0; j < kChunkSteps; ++j) {
+        const uint32_t wbase = c * kChunk + j * (uint32_t)R;
+        uint32_t next = wbase + (uint32_t)R;
+        if (j + 1 == kChunkSteps) {
+          cn = take(pend);
+          next = cn < nchunks ? cn * kChunk : wbase;
+        }
+        const uint32_t t = wbase + r;
+        process(exact, buf, t, t < nq, [&](uint2 (&dst)[NQ]) { load_rows(dst, seg_z, next, nq); });
       }
+      c = cn;
+      if (c < nchunks) pend = claim();
     }
-    __syncthreads();
-  });
+    flush_counts(plan.p);
+  }
   };
   if (keys_exact) sweep(std::true_type{});
   else sweep(std::false_type{});
@@ -784,13 +847,20 @@ __global__ __launch_bounds__(kBlock) void route_generic_kernel(
 }
 
 // ------------------------------------------------------------- launch ---
+// Dynamic tails only for blocks of at least this many block steps: on
+// shorter ranges the pool's claims cost more than the tail they remove
+// (E = 128 with 4,096 rows per block: 3% slower; E = 256 with 16,384: 2%
+// faster).
+constexpr int64_t kPoolMinSteps = 64;
+
 template <int E, int KT>
 void launch_fast(const RouteArgs& a, hipStream_t s) {
   int blocks;
   int64_t rpb;
   grid_for(a.T, kRouteWaves * (64 / FastCfg<E>::G), 1, &blocks, &rpb);
   route_fast_kernel<E, KT><<<blocks, kRouteBlock, 0, s>>>(a.z, a.b, a.T, a.K, a.idx, a.score, a.tau, a.load,
-                                                     a.hist, a.pt, rpb);
+                                                     a.hist, pool_table(a.pt, a.T, blocks, kPoolMinSteps * kRouteWaves * (64 / FastCfg<E>::G)),
+                                                     rpb);
 }
 
 template <int E>
@@ -812,8 +882,10 @@ eqb_status launch_route_e(const RouteArgs& a, hipStream_t s) {
     int blocks;
     int64_t rpb;
     grid_for(a.T, kWaves * (64 / (E / 8)), 1, &blocks, &rpb);
+    PartTable pt = a.pt;
+    pt.pool = nullptr;   // static ranges only
     route_generic_kernel<E><<<blocks, kBlock, 0, s>>>(a.z, a.b, a.T, a.K, a.idx, a.score, a.tau, a.load,
-                                                      a.hist, a.pt, rpb);
+                                                      a.hist, pt, rpb);
   }
   return launch_status();
 }

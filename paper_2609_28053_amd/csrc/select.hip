@@ -20,9 +20,12 @@ __global__ __launch_bounds__(kNBins) void select_coarse_kernel(
     int32_t* __restrict__ hist, int P, int E, int K, int64_t r, const PartTable pt,
     int32_t* __restrict__ sel_hi, int64_t* __restrict__ rank_in_bin, int32_t* __restrict__ hist_sum,
     int32_t* __restrict__ status, bool clear = false, int32_t* __restrict__ load_acc = nullptr,
-    int32_t* __restrict__ load_out = nullptr) {
+    int32_t* __restrict__ load_out = nullptr, int32_t* __restrict__ pool_reset = nullptr) {
   __shared__ int64_t sh[kNBins];
   const int e = blockIdx.x, u = threadIdx.x, p = kLocal ? (int)blockIdx.y : 0;
+  // the layer's claim counters of the sweep that ran before (one per partition)
+  if (pool_reset && e == 0)
+    for (int q = u; q < kPoolCounters; q += kNBins) pool_reset[(int64_t)q * kPoolStride] = 0;
   const int64_t out = kLocal ? (int64_t)p * E + e : e;
   if (kLocal) {
     const int64_t n = pt.off[p + 1] - pt.off[p];
@@ -66,9 +69,11 @@ __global__ __launch_bounds__(kNBins) void select_fine_kernel(
     int32_t* __restrict__ hist, int P, int E, const PartTable pt, const int32_t* __restrict__ sel_hi,
     const int64_t* __restrict__ rank_in_bin, int32_t* __restrict__ sel_lo,
     uint16_t* __restrict__ q_bf16, int32_t* __restrict__ hist_sum, int32_t* __restrict__ status,
-    bool clear = false) {
+    bool clear = false, int32_t* __restrict__ pool_reset = nullptr) {
   __shared__ int64_t sh[kNBins];
   const int e = blockIdx.x, v = threadIdx.x, p = kLocal ? (int)blockIdx.y : 0;
+  if (pool_reset && e == 0)
+    for (int q = v; q < kPoolCounters; q += kNBins) pool_reset[(int64_t)q * kPoolStride] = 0;
   const int64_t out = kLocal ? (int64_t)p * E + e : e;
   if (kLocal && pt.off[p + 1] == pt.off[p]) {
     if (v == 0) {
@@ -141,17 +146,17 @@ __global__ __launch_bounds__(256) void center_kernel(const uint16_t* __restrict_
 eqb_status launch_layer_selects(int pass, int32_t* hist, int P, int nsub, int E, int64_t r, int32_t* sel_hi,
                                 int64_t* rank_in_bin, int32_t* sel_lo, uint16_t* q_bf16, float* b_next,
                                 int32_t* hist_sum, int32_t* load_acc, int32_t* load_out, int32_t* status,
-                                hipStream_t s) {
+                                int32_t* pool_reset, hipStream_t s) {
   PartTable none{};
   none.P = P;
   const int nslabs = P * nsub;
   if (pass == 1) {
     select_coarse_kernel<false><<<E, kNBins, 0, s>>>(hist, nslabs, E, 0, r, none, sel_hi, rank_in_bin, hist_sum,
-                                                     nullptr, true, load_acc, load_out);
+                                                     nullptr, true, load_acc, load_out, pool_reset);
     return launch_status();
   }
   select_fine_kernel<false><<<E, kNBins, 0, s>>>(hist, nslabs, E, none, sel_hi, rank_in_bin, sel_lo, q_bf16,
-                                                 hist_sum, nullptr, true);
+                                                 hist_sum, nullptr, true, pool_reset);
   if (launch_status() != EQB_OK) return EQB_ERR_HIP;
   center_kernel<<<1, 256, 0, s>>>(q_bf16, E, b_next, sel_lo, status, sel_hi, rank_in_bin);
   return launch_status();
@@ -169,6 +174,7 @@ eqb_status launch_layer(const RouteArgs& route, int64_t r, const LayerWorkspace&
   a.load = w.load_acc;
   a.hist = w.hist_hi;
   a.pt.nsub = w.nsub;
+  a.pt.pool = w.pool;
   eqb_status st = mark(marks, 0, s);
   if (st != EQB_OK) return st;
   st = launch_route(a, s);
@@ -176,7 +182,7 @@ eqb_status launch_layer(const RouteArgs& route, int64_t r, const LayerWorkspace&
   if ((st = mark(marks, 1, s)) != EQB_OK) return st;
   const int P = a.pt.P, E = a.E;
   st = launch_layer_selects(1, w.hist_hi, P, w.nsub, E, r, w.sel_hi, w.rank_in_bin, nullptr, nullptr, nullptr,
-                            hist_hi_sum, w.load_acc, load_out, nullptr, s);
+                            hist_hi_sum, w.load_acc, load_out, nullptr, w.pool, s);
   if (st != EQB_OK) return st;
   if ((st = mark(marks, 2, s)) != EQB_OK) return st;
   MarginArgs m;
@@ -187,11 +193,12 @@ eqb_status launch_layer(const RouteArgs& route, int64_t r, const LayerWorkspace&
   m.sel_hi = w.sel_hi;
   m.hist = w.hist_lo;
   m.pt = a.pt;
+  m.pt.pool = nullptr;   // the fine pass keeps static ranges
   st = launch_margin(true, m, s);
   if (st != EQB_OK) return st;
   if ((st = mark(marks, 3, s)) != EQB_OK) return st;
   st = launch_layer_selects(2, w.hist_lo, P, w.nsub, E, r, w.sel_hi, w.rank_in_bin, w.sel_lo, q_bf16, b_next,
-                            hist_lo_sum, nullptr, nullptr, dev_status, s);
+                            hist_lo_sum, nullptr, nullptr, dev_status, nullptr, s);
   if (st != EQB_OK) return st;
   return mark(marks, 4, s);
 }

@@ -25,7 +25,7 @@ EQB_ERR_UNSUPPORTED = 2
 EQB_ERR_RANK = 3
 EQB_ERR_HIP = 4
 EQB_ERR_SCRATCH = 5
-EQB_NOALLOC_SCRATCH_BYTES = (8 << 20) + (64 << 10)
+EQB_NOALLOC_SCRATCH_BYTES = (8 << 20) + (192 << 10)
 EQB_NBINS = 256
 EQB_MAX_PARTITIONS = 256
 EQB_DEV_RANK_EXCEEDS_COUNT = 1

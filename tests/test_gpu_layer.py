@@ -106,3 +106,26 @@ def test_layer_equals_the_call_sequence(eqb):
         np.testing.assert_array_equal(got[k], ref[k])
     for k in ("tau", "score", "b_next"):
         np.testing.assert_array_equal(got[k].view(np.uint32), ref[k].view(np.uint32))
+
+
+# The one-call layer's route sweep takes its last rows as dynamic tails
+# (chunks that each block's waves claim once their own range is done) when a
+# block's range is long; a grid cap makes the ranges long at sizes the oracle
+# finishes quickly.  Groups of up to 16 blocks per partition, one or several
+# groups, partitions of unequal size and the hard rows (dry lanes, ties,
+# equal logits) of the routing tests.
+DYNAMIC = [("large256", 131072, 1, 16), ("large256", 262144, 1, 40), ("large256", 196608, 5, 24),
+           ("skew64", 262144, 3, 24), ("split128", 262144, 2, 34)]
+CUTS = {2: [0.58], 3: [0.30, 0.71], 5: [0.13, 0.41, 0.62, 0.85]}   # unequal partitions
+
+
+@pytest.mark.parametrize("name,T,P,cap", DYNAMIC, ids=[f"{d[0]}-P{d[2]}-cap{d[3]}" for d in DYNAMIC])
+def test_layer_dynamic_tails(eqb, name, T, P, cap):
+    w = W.WORKLOADS[name].with_T(T, P)
+    z, b, off = W.generate(w)
+    if P > 1:
+        off = np.array([0] + [int(T * f) for f in CUTS[P]] + [T], np.int64)
+    say(f"dynamic tails {name} T={T} E={w.E} K={w.K} P={P} grid cap {cap}")
+    want = O.run_layer(z, b, w.K, off, threads=8)
+    for got in run_twice(eqb, z, b, w.K, off, cap=cap):
+        check(got, want, w.K)

@@ -113,6 +113,24 @@ def test_parity_full_size(eqb, name):
     for k in ("H", "L", "u", "v", "rho", "bhat", "b_next", "idx", "tau"):
         np.testing.assert_array_equal(one[k], got[k])
     np.testing.assert_array_equal(one["load"][0], got["load"].sum(0))
+    # the one-call layer (dynamic tails, several count slabs per partition),
+    # twice on one workspace, at the size and launch configuration the bench
+    # times
+    say(f"full {name}: one-call layer")
+    lay = eqb.Layer(w.T, w.E, w.K, w.P)
+    zt = torch.from_numpy(np.ascontiguousarray(z).view(np.int16)).cuda()
+    bt = torch.from_numpy(np.ascontiguousarray(b, np.float32)).cuda()
+    po = eqb.PartOffsets([int(x) for x in off])
+    for _ in range(2):
+        lay.step(zt, bt, po, sums=True)
+        res = lay.step_results()
+        assert res["dev_status"] == 0 and res["workspace_zero"]
+        for k in ("idx", "load", "H", "L", "bhat"):
+            np.testing.assert_array_equal(np.asarray(res[k]), np.asarray(want[k]), err_msg=k)
+        np.testing.assert_array_equal(res["tau"].view(np.uint32), want["tau"].view(np.uint32))
+        np.testing.assert_array_equal(res["b_next"].view(np.uint32), want["b_next"].view(np.uint32))
+        ws = want["score"].astype(np.float64)
+        assert np.all(np.abs(res["score"].astype(np.float64) - ws) <= SCORE_RTOL * np.abs(ws))
 
 
 # ------------------------------------------------------------ edge cases --
