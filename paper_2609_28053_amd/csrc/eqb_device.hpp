@@ -413,8 +413,8 @@ __device__ __forceinline__ void block_rows(int64_t T, int64_t rows_per_block, in
 // left.  Groups keep the claims on one counter few.  Static ranges are
 // flushed every kSegPool rows, so a block's last static segment plus any pool
 // rows it takes stay below the 16-bit LDS counters' limit.
-constexpr int64_t kPoolMax = 16384;
-constexpr int64_t kPoolDiv = 12;
+constexpr int64_t kPoolMax = 32768;
+constexpr int64_t kPoolDiv = 8;
 constexpr int kGroupBlocks = 16;
 constexpr int64_t kSegPool = kSegMax - kPoolMax;
 // A group's claim counter is indexed by the group's first block and sits on

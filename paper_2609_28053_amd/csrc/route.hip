@@ -722,7 +722,7 @@ __global__ __launch_bounds__(kRouteBlock) void route_fast_kernel(
     // refill loads the next chunk's first rows; that read waits only for
     // loads the step waits for anyway.  A wave that draws past the pool
     // marks it spent in LDS, and the block's other waves then stop claiming.
-    constexpr uint32_t kChunkSteps = 16;
+    constexpr uint32_t kChunkSteps = 8;
     constexpr uint32_t kChunk = (uint32_t)R * kChunkSteps;
     set_base(plan.q0);
     const uint32_t nq = (uint32_t)(plan.q1 - plan.q0);
