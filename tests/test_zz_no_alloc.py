@@ -66,6 +66,22 @@ def test_noalloc_layer_matches_the_workspace_layer(eqb):
             np.testing.assert_array_equal(got[k].view(np.uint8), ref[k].view(np.uint8), err_msg=f"{name} {k}")
 
 
+def test_noalloc_layer_with_dynamic_tails(eqb):
+    # a grid of 16 blocks makes each block's range long enough for the route
+    # sweep's dynamic tails (claim counters in the scratch array, which the
+    # coarse selection resets); one partition, so 16 count slabs per
+    # partition; then a smaller layer and the first one again
+    try:
+        eqb.eqb_set_max_blocks(16)
+        for name, T, P in (("large256", 131072, 1), ("skew64", 7001, 4), ("large256", 131072, 1)):
+            ref, got = run_both(eqb, name, T, P)
+            assert int(ref["status"][0]) == 0 and int(got["status"][0]) == 0
+            for k in ref:
+                np.testing.assert_array_equal(got[k].view(np.uint8), ref[k].view(np.uint8), err_msg=f"{name} {k}")
+    finally:
+        eqb.eqb_set_max_blocks(0)
+
+
 def test_noalloc_layer_rejects_a_layer_beyond_its_scratch(eqb):
     w = W.WORKLOADS["large256"].with_T(4096, 17)        # P * E = 4352 > 4096
     z, b, off = W.generate(w)
