@@ -266,14 +266,17 @@ eqb_status eqb_lei_router_backward(const uint16_t* z, const int32_t* topk_idx, c
  *   dev_status [1] int32 (out, WRITTEN): EQB_DEV_OK, or
  *     EQB_DEV_RANK_EXCEEDS_COUNT when some expert's selection failed.
  *   workspace: device memory of at least eqb_layer_workspace_size(E, P)
- *     bytes, 256-byte aligned, owned by the caller.  It holds the
- *     per-partition counts and the selections while the layer runs.  It must
- *     be ALL ZERO when the call's work starts, and the call's work leaves it
- *     all zero again (each selection clears the counts it has summed), so a
- *     caller zeroes it once after allocating it and may then run layer after
- *     layer with it.  After an error reported by the call or by the runtime
- *     while its work ran, zero it again before the next use.  Two calls whose
- *     work may overlap need two workspaces.
+ *     bytes, 256-byte aligned, owned by the caller.  Its first
+ *     eqb_layer_workspace_zero_bytes(E, P) bytes hold the per-partition
+ *     counts and the selections while the layer runs: they must be ALL ZERO
+ *     when the call's work starts, and the call's work leaves them all zero
+ *     again (each selection clears the counts it has summed).  The rest is
+ *     scratch for the fine pass's per-block count images, which every call
+ *     overwrites before reading; its contents do not matter.  So a caller
+ *     zeroes the workspace once after allocating it and may then run layer
+ *     after layer with it.  After an error reported by the call or by the
+ *     runtime while its work ran, zero it again before the next use.  Two
+ *     calls whose work may overlap need two workspaces.
  *   marks (nullable): host array of 5 hipEvent_t handles, each nullable,
  *     recorded on `stream` before the route kernel, after it, after the
  *     coarse selection, after the fine pass and after the last kernel (for
@@ -282,7 +285,8 @@ eqb_status eqb_lei_router_backward(const uint16_t* z, const int32_t* topk_idx, c
  * null pointer or a workspace that is too small, EQB_ERR_UNSUPPORTED for a
  * misaligned z or workspace; other errors as for the calls it chains.
  */
-size_t eqb_layer_workspace_size(int32_t E, int32_t P);   /* host only; 0 for unsupported E or P */
+size_t eqb_layer_workspace_size(int32_t E, int32_t P);        /* host only; 0 for unsupported E or P */
+size_t eqb_layer_workspace_zero_bytes(int32_t E, int32_t P);  /* host only; 0 for unsupported E or P */
 eqb_status eqb_layer(const uint16_t* z, const float* b, int64_t T, int32_t E, int32_t K,
                      const int64_t* part_off, int32_t P, int32_t* topk_idx, float* topk_score, float* tau,
                      int32_t* load, uint16_t* q_bf16, float* b_next, int32_t* hist_hi_sum,
@@ -296,8 +300,10 @@ eqb_status eqb_layer(const uint16_t* z, const float* b, int64_t T, int32_t E, in
  * live in a library-owned device array of EQB_NOALLOC_SCRATCH_BYTES per GPU
  * (held until the process ends) instead of a caller workspace.  The call
  * allocates nothing; the caller still passes every input and output.
- *   Limit: eqb_layer_workspace_size(E, P) <= EQB_NOALLOC_SCRATCH_BYTES, i.e.
- *   P * E <= 4096 (E = 256: up to 16 partitions); larger layers return
+ *   The array holds the layer's counters only (the fine pass adds its counts
+ *   to the partition slabs instead of storing per-block images).
+ *   Limit: eqb_layer_workspace_zero_bytes(E, P) <= EQB_NOALLOC_SCRATCH_BYTES,
+ *   i.e. P * E <= 4096 (E = 256: up to 16 partitions); larger layers return
  *   EQB_ERR_SCRATCH before anything is enqueued.
  *   Every call on one GPU shares that GPU's array: the call clears the part
  *   it uses (a fill kernel) before the layer runs, and calls whose work may

@@ -280,11 +280,31 @@ size_t eqb_layer_workspace_size(int32_t E, int32_t P) {
   return layer_workspace(nullptr, E, P, nullptr);
 }
 
+size_t eqb_layer_workspace_zero_bytes(int32_t E, int32_t P) {
+  if (!supported_E(E) || P < 1 || P > EQB_MAX_PARTITIONS) return 0;
+  size_t zero = 0;
+  layer_workspace(nullptr, E, P, nullptr, true, &zero);
+  return zero;
+}
+
 eqb_status eqb_layer(const uint16_t* z, const float* b, int64_t T, int32_t E, int32_t K,
                      const int64_t* part_off, int32_t P, int32_t* topk_idx, float* topk_score, float* tau,
                      int32_t* load, uint16_t* q_bf16, float* b_next, int32_t* hist_hi_sum,
                      int32_t* hist_lo_sum, int32_t* dev_status, void* workspace, size_t workspace_bytes,
                      void* const* marks, void* stream) {
+  return layer_call(z, b, T, E, K, part_off, P, topk_idx, topk_score, tau, load, q_bf16, b_next, hist_hi_sum,
+                    hist_lo_sum, dev_status, workspace, workspace_bytes, true, marks, stream);
+}
+
+}  // extern "C"
+
+namespace eqb {
+
+eqb_status layer_call(const uint16_t* z, const float* b, int64_t T, int32_t E, int32_t K,
+                      const int64_t* part_off, int32_t P, int32_t* topk_idx, float* topk_score, float* tau,
+                      int32_t* load, uint16_t* q_bf16, float* b_next, int32_t* hist_hi_sum,
+                      int32_t* hist_lo_sum, int32_t* dev_status, void* workspace, size_t workspace_bytes,
+                      bool with_part, void* const* marks, void* stream) {
   if (T < 0 || T > INT32_MAX || K < 1 || K >= E) return EQB_ERR_INVALID_ARG;
   if (!supported_E(E)) return EQB_ERR_UNSUPPORTED;
   RouteArgs a;
@@ -297,7 +317,7 @@ eqb_status eqb_layer(const uint16_t* z, const float* b, int64_t T, int32_t E, in
   if (!aligned16(z)) return EQB_ERR_UNSUPPORTED;
   if (reinterpret_cast<uintptr_t>(workspace) % 256 != 0) return EQB_ERR_UNSUPPORTED;
   LayerWorkspace w;
-  if (workspace_bytes < layer_workspace(workspace, E, a.pt.P, &w)) return EQB_ERR_INVALID_ARG;
+  if (workspace_bytes < layer_workspace(workspace, E, a.pt.P, &w, with_part)) return EQB_ERR_INVALID_ARG;
   a.z = z;
   a.b = b;
   a.T = T;
@@ -309,6 +329,10 @@ eqb_status eqb_layer(const uint16_t* z, const float* b, int64_t T, int32_t E, in
   return launch_layer(a, r, w, q_bf16, b_next, load, hist_hi_sum, hist_lo_sum, dev_status, marks,
                       static_cast<hipStream_t>(stream));
 }
+
+}  // namespace eqb
+
+extern "C" {
 
 eqb_status eqb_set_max_blocks(int32_t max_blocks) {
   if (max_blocks < 0) return EQB_ERR_INVALID_ARG;

@@ -27,10 +27,31 @@ struct MarginArgs {
   int sel_stride = 0;      // 0: one selection for all partitions; E: one per partition
   int32_t* hist;
   PartTable pt;
+  // Fine pass of a layer (sel_stride 0, counts summed over partitions): room
+  // for part_blocks per-block images of the LDS counts (part_words(E) words
+  // each).  When the pass's grid fits (at most part_blocks blocks, at most
+  // kSegMax rows per block) every block stores its counts there with plain
+  // stores instead of adding them to `hist`.
+  uint32_t* part = nullptr;
+  int part_blocks = 0;
 };
 
+// Words of one block's image of the fine counts: for each expert pair
+// (2m, 2m+1), 256 words holding the two experts' 16-bit counts of raw low
+// byte j in their low and high halves.
+__host__ __device__ inline int64_t part_words(int E) { return (int64_t)(E / 2) * kNBins; }
+// Blocks of the fine pass per compute unit (its LDS counts take (E/2) * 257
+// words per block) and the per-block images a layer workspace holds: enough
+// for one full grid on a device of up to 256 compute units (a larger device
+// runs the pass with fewer, longer blocks).
+inline int margin_blocks_per_cu(int E) { return (E / 2) * kHistStride * 4 * 2 <= 160 * 1024 ? 2 : 1; }
+constexpr int kPartCUs = 256;
+inline int layer_part_blocks(int E) { return kPartCUs * margin_blocks_per_cu(E); }
+
 eqb_status launch_route(const RouteArgs& a, hipStream_t s);
-eqb_status launch_margin(bool fine, const MarginArgs& a, hipStream_t s);
+// *part_used: the number of per-block images the fine pass wrote (0 when it
+// added its counts to a.hist).
+eqb_status launch_margin(bool fine, const MarginArgs& a, hipStream_t s, int* part_used = nullptr);
 eqb_status launch_load(const int32_t* idx, int64_t T, int K, int E, int32_t* load, const PartTable& pt,
                        hipStream_t s);
 eqb_status launch_select(int pass, const int32_t* hist, int P, int E, int64_t r, int32_t* sel_hi,
@@ -41,6 +62,11 @@ eqb_status launch_layer_selects(int pass, int32_t* hist, int P, int nsub, int E,
                                 int64_t* rank_in_bin, int32_t* sel_lo, uint16_t* q_bf16, float* b_next,
                                 int32_t* hist_sum, int32_t* load_acc, int32_t* load_out, int32_t* status,
                                 int32_t* pool_reset, hipStream_t s);
+// The fine selection of a layer from the fine pass's per-block images
+// (nparts of them), then the centring and status as launch_layer_selects(2).
+eqb_status launch_layer_select_parts(const uint32_t* part, int nparts, int E, int32_t* sel_hi,
+                                     int64_t* rank_in_bin, int32_t* sel_lo, uint16_t* q_bf16, float* b_next,
+                                     int32_t* hist_sum, int32_t* status, hipStream_t s);
 
 eqb_status launch_select_local(int pass, const int32_t* hist, int E, int K, const PartTable& pt,
                                int32_t* sel_hi, int64_t* rank_in_bin, int32_t* sel_lo, uint16_t* q_bf16,
@@ -69,9 +95,12 @@ inline int layer_replicas(int P) { return P >= 16 ? 1 : 16 / P; }
 
 // Working buffers of one layer (eqb_layer): the per-partition coarse and
 // fine counts (layer_replicas(P) slabs per partition), the loads as the
-// route kernel accumulates them, and the selections.  Each piece starts on a
-// 256-byte boundary.  The counters are zero when a layer starts and zero
-// again when it ends: the selection that reads a counter clears it.
+// route kernel accumulates them, the selections, and (optionally) room for
+// the fine pass's per-block count images.  Each piece starts on a 256-byte
+// boundary.  The counters (everything before the images) are zero when a
+// layer starts and zero again when it ends: the selection that reads a
+// counter clears it.  The images are scratch: the fine pass overwrites the
+// ones the fine selection reads.
 struct LayerWorkspace {
   int nsub;               // count slabs per partition
   int32_t* hist_hi;       // [P,nsub,E,256]
@@ -81,19 +110,26 @@ struct LayerWorkspace {
   int32_t* sel_lo;        // [E]
   int64_t* rank_in_bin;   // [E]
   int32_t* pool;          // claim counters of the route sweep's dynamic tails (kPoolCounters, kPoolStride apart)
+  uint32_t* part;         // [part_blocks, part_words(E)] or null
+  int part_blocks;
 };
 
 inline size_t align256(size_t n) { return (n + 255) & ~(size_t)255; }
 
 // Bytes of a layer workspace, and its pieces carved from base (null base:
-// only the size is computed).
-inline size_t layer_workspace(void* base, int E, int P, LayerWorkspace* w) {
+// only the size is computed).  with_part = false leaves out the fine pass's
+// images (the layer then adds the fine counts to the slabs); *zero_bytes
+// (nullable) receives the size of the leading part that holds the counters.
+inline size_t layer_workspace(void* base, int E, int P, LayerWorkspace* w, bool with_part = true,
+                              size_t* zero_bytes = nullptr) {
   const int nsub = layer_replicas(P);
   const size_t hist = align256((size_t)P * nsub * E * kNBins * sizeof(int32_t));
   const size_t load = align256((size_t)P * E * sizeof(int32_t));
   const size_t sel = align256((size_t)E * sizeof(int32_t));
   const size_t rib = align256((size_t)E * sizeof(int64_t));
   const size_t pool = (size_t)kPoolCounters * kPoolStride * sizeof(int32_t);
+  const size_t zero = 2 * hist + load + 2 * sel + rib + pool;
+  const size_t part = with_part ? align256((size_t)layer_part_blocks(E) * part_words(E) * sizeof(uint32_t)) : 0;
   if (base && w) {
     char* p = static_cast<char*>(base);
     w->nsub = nsub;
@@ -104,9 +140,20 @@ inline size_t layer_workspace(void* base, int E, int P, LayerWorkspace* w) {
     w->sel_lo = reinterpret_cast<int32_t*>(p + 2 * hist + load + sel);
     w->rank_in_bin = reinterpret_cast<int64_t*>(p + 2 * hist + load + 2 * sel);
     w->pool = reinterpret_cast<int32_t*>(p + 2 * hist + load + 2 * sel + rib);
+    w->part = with_part ? reinterpret_cast<uint32_t*>(p + zero) : nullptr;
+    w->part_blocks = with_part ? layer_part_blocks(E) : 0;
   }
-  return 2 * hist + load + 2 * sel + rib + pool;
+  if (zero_bytes) *zero_bytes = zero;
+  return zero + part;
 }
+
+// eqb_layer with the workspace layout chosen by with_part (the fine pass's
+// per-block images present or not; see layer_workspace).
+eqb_status layer_call(const uint16_t* z, const float* b, int64_t T, int32_t E, int32_t K,
+                      const int64_t* part_off, int32_t P, int32_t* topk_idx, float* topk_score, float* tau,
+                      int32_t* load, uint16_t* q_bf16, float* b_next, int32_t* hist_hi_sum,
+                      int32_t* hist_lo_sum, int32_t* dev_status, void* workspace, size_t workspace_bytes,
+                      bool with_part, void* const* marks, void* stream);
 
 // The whole layer on one stream: route + loads + coarse counts, coarse
 // selection (clearing the coarse counts, handing the loads out), fine

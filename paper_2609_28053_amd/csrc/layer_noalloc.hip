@@ -53,8 +53,12 @@ extern "C" eqb_status eqb_layer_noalloc(const uint16_t* z, const float* b, int64
                                         float* topk_score, float* tau, int32_t* load, uint16_t* q_bf16,
                                         float* b_next, int32_t* hist_hi_sum, int32_t* hist_lo_sum,
                                         int32_t* dev_status, void* stream) {
-  // the argument checks of eqb_layer, except the workspace's
-  const size_t need = eqb_layer_workspace_size(E, part_off ? P : 1);
+  // the argument checks of eqb_layer, except the workspace's.  The array
+  // holds the layer's counters only: the fine pass adds its counts to the
+  // partition slabs instead of storing per-block images.
+  size_t need = 0;
+  if (eqb_layer_workspace_size(E, part_off ? P : 1) != 0)
+    need = layer_workspace(nullptr, E, part_off ? P : 1, nullptr, false);
   if (need > kScratchBytes) return EQB_ERR_SCRATCH;
   if (T < 0 || T > INT32_MAX || K < 1 || K >= E) return EQB_ERR_INVALID_ARG;
   if (need == 0) return (E == 8 || E == 16 || E == 32 || E == 64 || E == 128 || E == 256) ?
@@ -73,6 +77,6 @@ extern "C" eqb_status eqb_layer_noalloc(const uint16_t* z, const float* b, int64
   const int blocks = (int)((n16 + 255) / 256 < 1024 ? (n16 + 255) / 256 : 1024);
   zero_kernel<<<blocks, 256, 0, s>>>(static_cast<uint4*>(ws), n16);
   if (launch_status() != EQB_OK) return EQB_ERR_HIP;
-  return eqb_layer(z, b, T, E, K, part_off, P, topk_idx, topk_score, tau, load, q_bf16, b_next, hist_hi_sum,
-                   hist_lo_sum, dev_status, ws, need, nullptr, stream);
+  return layer_call(z, b, T, E, K, part_off, P, topk_idx, topk_score, tau, load, q_bf16, b_next, hist_hi_sum,
+                    hist_lo_sum, dev_status, ws, need, false, nullptr, stream);
 }

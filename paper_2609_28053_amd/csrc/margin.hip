@@ -13,6 +13,7 @@
 namespace eqb {
 
 constexpr int kMarginU = 3;   // rows per lane per block step
+constexpr int kPartMinRows = 512;    // least rows per block when the blocks store count images
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
 // Counts the margins of one row piece: eight experts e0 .. e0+7 (four packed
@@ -44,11 +45,17 @@ __device__ __forceinline__ void count_piece(uint32_t* sh, const uint4& w, float 
 // sel_stride = 0: every partition uses the selection sel_hi[e] (EQB: the
 // bins chosen from the summed counts).  sel_stride = E: partition p uses its
 // own selection sel_hi[p*E + e] (each shard's own quantile).
+// part (fine pass with sel_stride 0, at most kSegMax rows per block): the
+// block's counts, summed over the partitions it covers, are stored as one
+// image of part_words(E) words at part + blockIdx.x * part_words(E) (plain
+// stores; the fine selection sums the images) instead of being added to the
+// partition slabs, whose atomics queue in the memory system when every block
+// flushes at once.
 template <int E, bool kFine>
 __global__ __launch_bounds__(kBlock) void margin_hist_kernel(
     const uint16_t* __restrict__ z, const float* __restrict__ tau, int64_t T,
     const int32_t* __restrict__ sel_hi, int sel_stride, int32_t* __restrict__ hist, const PartTable pt,
-    int64_t rows_per_block) {
+    int64_t rows_per_block, uint32_t* __restrict__ part) {
   constexpr int G = E / 8;
   constexpr int R = 64 / G;
   constexpr int ROWS = kWaves * R * kMarginU;
@@ -124,6 +131,7 @@ __global__ __launch_bounds__(kBlock) void margin_hist_kernel(
         if (t < n) count_piece<kFine>(sh_hist, va[u], ta[u], row0, csel);
       }
     }
+    if (kFine && part) return;   // the counts stay in LDS until the block's image is stored
     __syncthreads();
     int32_t* slab = count_slab(hist, pt, p, E);
     if (!kFine) {
@@ -133,34 +141,51 @@ __global__ __launch_bounds__(kBlock) void margin_hist_kernel(
     }
     __syncthreads();
   });
+  if (kFine && part) {
+    __syncthreads();
+    // four words of one pair's row per thread: word m*257 + 4k.. in LDS,
+    // 16 bytes at m*256 + 4k in the image
+    uint4* dst = reinterpret_cast<uint4*>(part + (int64_t)blockIdx.x * part_words(E));
+    for (int it = threadIdx.x; it < (E / 2) * (kNBins / 4); it += kBlock) {
+      const uint32_t* src = sh_hist + (it / (kNBins / 4)) * kHistStride + 4 * (it % (kNBins / 4));
+      dst[it] = make_uint4(src[0], src[1], src[2], src[3]);
+    }
+  }
 }
 
 template <int E>
-eqb_status launch_margin_e(bool fine, const MarginArgs& a, hipStream_t s) {
+eqb_status launch_margin_e(bool fine, const MarginArgs& a, hipStream_t s, int* part_used) {
+  static_assert(hist_words<E>() == (E / 2) * kHistStride, "LDS counts as margin_blocks_per_cu assumes");
   int blocks;
   int64_t rpb;
   const int rows_per_step = kWaves * (64 / (E / 8)) * kMarginU;
-  // At least 1,024 rows per block: at one rank's share of the paper's batch
-  // (147,456 tokens, E = 256) that roughly halves the blocks whose LDS
-  // counts are zeroed and flushed; large batches still fill every CU.
-  grid_for(a.T, rows_per_step, hist_words<E>() * 4 * 2 <= 160 * 1024 ? 2 : 1, &blocks, &rpb,
-           (1024 + rows_per_step - 1) / rows_per_step);
+  // At least 1,024 rows per block when the counts are flushed with atomics:
+  // at one rank's share of the paper's batch (147,456 tokens, E = 256) that
+  // roughly halves the blocks whose LDS counts are zeroed and flushed; large
+  // batches still fill every CU.  Per-block images cost a block far less, so
+  // their blocks may be shorter.
+  const bool want_part = fine && a.part != nullptr && a.sel_stride == 0;
+  const int min_rows = want_part ? kPartMinRows : 1024;
+  grid_for(a.T, rows_per_step, margin_blocks_per_cu(E), &blocks, &rpb, (min_rows + rows_per_step - 1) / rows_per_step);
+  const bool use_part = want_part && blocks <= a.part_blocks && rpb <= kSegMax;
+  if (part_used) *part_used = use_part ? blocks : 0;
   if (fine)
     margin_hist_kernel<E, true><<<blocks, kBlock, 0, s>>>(a.z, a.tau, a.T, a.sel_hi, a.sel_stride, a.hist,
-                                                         a.pt, rpb);
+                                                         a.pt, rpb, use_part ? a.part : nullptr);
   else
-    margin_hist_kernel<E, false><<<blocks, kBlock, 0, s>>>(a.z, a.tau, a.T, a.sel_hi, 0, a.hist, a.pt, rpb);
+    margin_hist_kernel<E, false><<<blocks, kBlock, 0, s>>>(a.z, a.tau, a.T, a.sel_hi, 0, a.hist, a.pt, rpb,
+                                                          nullptr);
   return launch_status();
 }
 
-eqb_status launch_margin(bool fine, const MarginArgs& a, hipStream_t s) {
+eqb_status launch_margin(bool fine, const MarginArgs& a, hipStream_t s, int* part_used) {
   switch (a.E) {
-    case 8: return launch_margin_e<8>(fine, a, s);
-    case 16: return launch_margin_e<16>(fine, a, s);
-    case 32: return launch_margin_e<32>(fine, a, s);
-    case 64: return launch_margin_e<64>(fine, a, s);
-    case 128: return launch_margin_e<128>(fine, a, s);
-    case 256: return launch_margin_e<256>(fine, a, s);
+    case 8: return launch_margin_e<8>(fine, a, s, part_used);
+    case 16: return launch_margin_e<16>(fine, a, s, part_used);
+    case 32: return launch_margin_e<32>(fine, a, s, part_used);
+    case 64: return launch_margin_e<64>(fine, a, s, part_used);
+    case 128: return launch_margin_e<128>(fine, a, s, part_used);
+    case 256: return launch_margin_e<256>(fine, a, s, part_used);
     default: return EQB_ERR_UNSUPPORTED;
   }
 }

@@ -106,6 +106,93 @@ __global__ __launch_bounds__(kNBins) void select_fine_kernel(
   }
 }
 
+// The fine selection of a layer from the fine pass's per-block count images
+// (steps 5-6 of Algorithm 1 with the all-reduce stand-in summing the images
+// instead of partition slabs).  One block per expert pair (2m, 2m+1), 512
+// threads: each wave sums every eighth image's row for the pair (one
+// 16-byte load per lane: raw low bytes 4l..4l+3 of both experts), the waves'
+// sums meet in LDS, and threads 256x + v then hold kappa bin v of expert
+// 2m + x: raw low byte v, or v ^ 0xFF when the expert's selected coarse bin
+// holds negative margins (kappa flips every bit of a negative value).  The
+// scan and the choice are those of select_fine_kernel.  Image counts are
+// below 2^16 and the sums below 2^31 (T < 2^31).
+constexpr int kPartThreads = 512;
+__global__ __launch_bounds__(kPartThreads) void select_fine_parts_kernel(
+    const uint32_t* __restrict__ part, int nparts, int E, const int32_t* __restrict__ sel_hi,
+    const int64_t* __restrict__ rank_in_bin, int32_t* __restrict__ sel_lo, uint16_t* __restrict__ q_bf16,
+    int32_t* __restrict__ hist_sum) {
+  constexpr int kW = kPartThreads / 64;
+  __shared__ uint32_t sh[kW][2 * kNBins];   // per wave: raw bins of expert 2m, then of 2m+1
+  __shared__ int sh_tot[kW];
+  const int m = blockIdx.x, lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int64_t words = part_words(E);
+  const uint4* src = reinterpret_cast<const uint4*>(part + (int64_t)m * kNBins) + lane;
+  uint32_t lo[4] = {0, 0, 0, 0}, hi[4] = {0, 0, 0, 0};
+  int b = wave;
+  for (; b + 3 * kW < nparts; b += 4 * kW) {
+    uint4 v[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) v[j] = src[(b + j * kW) * words / 4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const uint32_t w[4] = {v[j].x, v[j].y, v[j].z, v[j].w};
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        lo[i] += w[i] & 0xFFFFu;
+        hi[i] += w[i] >> 16;
+      }
+    }
+  }
+  for (; b < nparts; b += kW) {
+    const uint4 v = src[b * words / 4];
+    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      lo[i] += w[i] & 0xFFFFu;
+      hi[i] += w[i] >> 16;
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    sh[wave][4 * lane + i] = lo[i];
+    sh[wave][kNBins + 4 * lane + i] = hi[i];
+  }
+  __syncthreads();
+  const int x = threadIdx.x >> 8, v = threadIdx.x & (kNBins - 1);
+  const int e = 2 * m + x;
+  const int u = sel_hi[e];
+  const int64_t rho = rank_in_bin[e];
+  const bool ok = u >= 0 && u < kNBins && rho >= 1;
+  const bool valid_u = u >= 0 && u < kNBins;
+  const int raw = (valid_u && u < 0x80) ? (v ^ 0xFF) : v;
+  int c = 0;
+#pragma unroll
+  for (int w = 0; w < kW; ++w) c += (int)sh[w][x * kNBins + raw];
+  // the fine pass counted an expert without a valid coarse choice in bin 0;
+  // like the slab flush, the selection drops those counts
+  if (!valid_u) c = 0;
+  if (hist_sum) hist_sum[(int64_t)e * kNBins + v] = c;
+  // inclusive scan over the 256 threads of expert x (waves 4x .. 4x+3)
+  int y = c;
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    const int t = __shfl_up(y, d);
+    if (lane >= d) y += t;
+  }
+  if (lane == 63) sh_tot[wave] = y;
+  __syncthreads();
+  for (int w = 4 * x; w < wave; ++w) y += sh_tot[w];
+  const int64_t cum = y;
+  if (ok && cum >= rho && cum - c < rho) {
+    sel_lo[e] = v;
+    q_bf16[e] = kappa_inv(((uint32_t)u << 8) | (uint32_t)v);
+  }
+  if (v == kNBins - 1 && (!ok || cum < rho)) {
+    sel_lo[e] = -1;
+    q_bf16[e] = 0x7FC0;
+  }
+}
+
 // b = b_hat - mean(b_hat): binary64 sum in ascending expert order, divided by
 // E, difference in binary64, one rounding to binary32.  With status_out (the
 // layer form) the kernel also writes the layer's status (an expert whose fine
@@ -162,6 +249,16 @@ eqb_status launch_layer_selects(int pass, int32_t* hist, int P, int nsub, int E,
   return launch_status();
 }
 
+eqb_status launch_layer_select_parts(const uint32_t* part, int nparts, int E, int32_t* sel_hi,
+                                     int64_t* rank_in_bin, int32_t* sel_lo, uint16_t* q_bf16, float* b_next,
+                                     int32_t* hist_sum, int32_t* status, hipStream_t s) {
+  select_fine_parts_kernel<<<E / 2, kPartThreads, 0, s>>>(part, nparts, E, sel_hi, rank_in_bin, sel_lo, q_bf16,
+                                                          hist_sum);
+  if (launch_status() != EQB_OK) return EQB_ERR_HIP;
+  center_kernel<<<1, 256, 0, s>>>(q_bf16, E, b_next, sel_lo, status, sel_hi, rank_in_bin);
+  return launch_status();
+}
+
 static eqb_status mark(void* const* marks, int i, hipStream_t s) {
   if (marks == nullptr || marks[i] == nullptr) return EQB_OK;
   return hipEventRecord(static_cast<hipEvent_t>(marks[i]), s) == hipSuccess ? EQB_OK : EQB_ERR_HIP;
@@ -194,11 +291,18 @@ eqb_status launch_layer(const RouteArgs& route, int64_t r, const LayerWorkspace&
   m.hist = w.hist_lo;
   m.pt = a.pt;
   m.pt.pool = nullptr;   // the fine pass keeps static ranges
-  st = launch_margin(true, m, s);
+  m.part = w.part;
+  m.part_blocks = w.part_blocks;
+  int nparts = 0;
+  st = launch_margin(true, m, s, &nparts);
   if (st != EQB_OK) return st;
   if ((st = mark(marks, 3, s)) != EQB_OK) return st;
-  st = launch_layer_selects(2, w.hist_lo, P, w.nsub, E, r, w.sel_hi, w.rank_in_bin, w.sel_lo, q_bf16, b_next,
-                            hist_lo_sum, nullptr, nullptr, dev_status, nullptr, s);
+  if (nparts > 0)
+    st = launch_layer_select_parts(w.part, nparts, E, w.sel_hi, w.rank_in_bin, w.sel_lo, q_bf16, b_next,
+                                   hist_lo_sum, dev_status, s);
+  else
+    st = launch_layer_selects(2, w.hist_lo, P, w.nsub, E, r, w.sel_hi, w.rank_in_bin, w.sel_lo, q_bf16, b_next,
+                              hist_lo_sum, nullptr, nullptr, dev_status, nullptr, s);
   if (st != EQB_OK) return st;
   return mark(marks, 4, s);
 }

@@ -46,6 +46,7 @@ EXPORTS = (
     "eqb_lei_inject",
     "eqb_lei_router_backward",
     "eqb_layer_workspace_size",
+    "eqb_layer_workspace_zero_bytes",
     "eqb_layer",
     "eqb_layer_noalloc",
     "eqb_set_max_blocks",
@@ -80,6 +81,7 @@ def _load():
         "eqb_lei_inject": [P, P, i64, i32, P, i32, P],
         "eqb_lei_router_backward": [P, P, P, P, i64, i32, i32, P, i32, P, P],
         "eqb_layer_workspace_size": [i32, i32],
+        "eqb_layer_workspace_zero_bytes": [i32, i32],
         "eqb_layer": [P, P, i64, i32, i32, P, i32, P, P, P, P, P, P, P, P, P, P, ctypes.c_size_t, P, P],
         "eqb_layer_noalloc": [P, P, i64, i32, i32, P, i32, P, P, P, P, P, P, P, P, P, P],
         "eqb_set_max_blocks": [i32],
@@ -93,6 +95,7 @@ def _load():
         fn.restype = i32
     lib.eqb_rank.restype = i64
     lib.eqb_layer_workspace_size.restype = ctypes.c_size_t
+    lib.eqb_layer_workspace_zero_bytes.restype = ctypes.c_size_t
     lib.eqb_status_string.restype = ctypes.c_char_p
     return lib
 
@@ -316,6 +319,12 @@ def eqb_layer_workspace_size(E: int, P: int) -> int:
     return int(lib.eqb_layer_workspace_size(E, P))
 
 
+def eqb_layer_workspace_zero_bytes(E: int, P: int) -> int:
+    """Leading bytes of a layer workspace that hold its counters (zero
+    before and after every call); the rest is the fine pass's scratch."""
+    return int(lib.eqb_layer_workspace_zero_bytes(E, P))
+
+
 def layer_marks(events):
     """The marks argument of eqb_layer from five torch.cuda.Event objects (or
     None entries).  An event's handle exists once it has been recorded, so
@@ -429,7 +438,13 @@ class Layer:
         g = lambda t: t.cpu().numpy()
         return dict(idx=g(self.topk_idx), score=g(self.topk_score), tau=g(self.tau), load=g(self.load_out),
                     H=g(self.H), L=g(self.L), bhat=g(self.q_bf16).view(np.uint16), b_next=g(self.b_next),
-                    dev_status=int(self.status.item()), workspace_zero=bool((self.workspace == 0).all().item()))
+                    dev_status=int(self.status.item()), workspace_zero=self.counters_zero())
+
+    def counters_zero(self) -> bool:
+        """Whether the counter part of the layer workspace is all zero (as
+        every call must leave it)."""
+        n = eqb_layer_workspace_zero_bytes(self.E, self.P)
+        return bool((self.workspace[:n] == 0).all().item())
 
     def run(self, z, b, part_off=None, fused=True, stream=None):
         """One layer: route (+ coarse counts), select 1, fine counts, select 2."""

@@ -36,6 +36,8 @@ def lib():
     lib.eqb_lei_router_backward.argtypes = [V, V, V, V, i64, i32, i32, V, i32, V, V]
     lib.eqb_layer_workspace_size.argtypes = [i32, i32]
     lib.eqb_layer_workspace_size.restype = ctypes.c_size_t
+    lib.eqb_layer_workspace_zero_bytes.argtypes = [i32, i32]
+    lib.eqb_layer_workspace_zero_bytes.restype = ctypes.c_size_t
     lib.eqb_layer.argtypes = [V, V, i64, i32, i32, V, i32] + [V] * 10 + [ctypes.c_size_t, V, V]
     lib.eqb_set_max_blocks.argtypes = [i32]
     lib.eqb_get_max_blocks.argtypes = []
@@ -196,18 +198,24 @@ def layer(lib, T=64, E=8, K=2, ws=ctypes.c_void_p(0x10000), ws_bytes=1 << 30, po
 
 
 def test_layer_workspace_size(lib):
-    # two sets of [P,nsub,E,256] int32 count slabs (nsub = 16 // P slabs per
-    # partition below 16 partitions, else 1), the [P,E] loads and three [E]
-    # selections, each rounded up to 256 bytes, and 1,024 claim counters of
-    # the route sweep's dynamic tails, 128 bytes apart
+    # Counters: two sets of [P,nsub,E,256] int32 count slabs (nsub = 16 // P
+    # slabs per partition below 16 partitions, else 1), the [P,E] loads and
+    # three [E] selections, each rounded up to 256 bytes, and 1,024 claim
+    # counters of the route sweep's dynamic tails, 128 bytes apart.  Then the
+    # fine pass's per-block images, E/2 * 256 words each, for one or two
+    # blocks per compute unit (two when two blocks' LDS counts, (E/2) * 257
+    # words each, fit in 160 KiB) on 256 compute units.
     for E, P in ((8, 1), (64, 4), (128, 3), (256, 1), (256, 16), (256, 17), (256, 256)):
         nsub = 1 if P >= 16 else 16 // P
-        want = (2 * P * nsub * E * 1024 + -(-4 * P * E // 256) * 256 + 2 * -(-4 * E // 256) * 256
+        zero = (2 * P * nsub * E * 1024 + -(-4 * P * E // 256) * 256 + 2 * -(-4 * E // 256) * 256
                 + -(-8 * E // 256) * 256 + 1024 * 128)
-        assert lib.eqb_layer_workspace_size(E, P) == want
-    assert lib.eqb_layer_workspace_size(12, 1) == 0
-    assert lib.eqb_layer_workspace_size(8, 0) == 0
-    assert lib.eqb_layer_workspace_size(8, 257) == 0
+        blocks = 256 * (2 if (E // 2) * 257 * 4 * 2 <= 160 * 1024 else 1)
+        assert lib.eqb_layer_workspace_zero_bytes(E, P) == zero
+        assert lib.eqb_layer_workspace_size(E, P) == zero + blocks * (E // 2) * 256 * 4
+    assert lib.eqb_layer_workspace_size(256, 1) - lib.eqb_layer_workspace_zero_bytes(256, 1) == 32 << 20
+    for E, P in ((12, 1), (8, 0), (8, 257)):
+        assert lib.eqb_layer_workspace_size(E, P) == 0
+        assert lib.eqb_layer_workspace_zero_bytes(E, P) == 0
 
 
 def test_layer_argument_checks(lib):

@@ -1,10 +1,11 @@
 """GPU parity of the one-call layer (eqb_layer) against the CPU oracle.
 
 eqb_layer chains the route kernel, both selections and the fine pass with a
-caller-owned workspace that must be zero when a layer starts and is left zero
-when it ends (each selection clears the counts it has summed).  Every layer
-below runs twice on the same workspace: the second run can only match the
-oracle if the first left the workspace zeroed.
+caller-owned workspace whose counter part must be zero when a layer starts
+and is left zero when it ends (each selection clears the counts it has
+summed); the rest is scratch for the fine pass's per-block count images.
+Every layer below runs twice on the same workspace: the second run can only
+match the oracle if the first left the counters zeroed.
 """
 import sys
 
@@ -34,7 +35,7 @@ def say(msg):
 
 def check(got, want, K):
     assert got["dev_status"] == 0
-    assert got["workspace_zero"], "the layer must leave its workspace zeroed"
+    assert got["workspace_zero"], "the layer must leave its workspace counters zeroed"
     np.testing.assert_array_equal(got["idx"], want["idx"])
     np.testing.assert_array_equal(got["tau"].view(np.uint32), want["tau"].view(np.uint32))
     ws = want["score"].astype(np.float64)
@@ -128,4 +129,41 @@ def test_layer_dynamic_tails(eqb, name, T, P, cap):
     say(f"dynamic tails {name} T={T} E={w.E} K={w.K} P={P} grid cap {cap}")
     want = O.run_layer(z, b, w.K, off, threads=8)
     for got in run_twice(eqb, z, b, w.K, off, cap=cap):
+        check(got, want, w.K)
+
+
+def test_layer_scratch_contents_do_not_matter(eqb):
+    """Past eqb_layer_workspace_zero_bytes the workspace is scratch for the
+    fine pass's per-block count images: filled with ones before each call,
+    the layer still matches the oracle and leaves its counters zero."""
+    w = W.WORKLOADS["split128"].with_T(40009, 3)
+    z, b, off = W.generate(w)
+    want = O.run_layer(z, b, w.K, off, threads=8)
+    zt = torch.from_numpy(z.view(np.int16)).cuda()
+    bt = torch.from_numpy(b).cuda()
+    po = eqb.PartOffsets([int(x) for x in off])
+    lay = eqb.Layer(w.T, w.E, w.K, w.P)
+    lay._layer_buffers()
+    n = eqb.eqb_layer_workspace_zero_bytes(w.E, w.P)
+    assert 0 < n < lay.workspace.numel()
+    for i in range(2):
+        say(f"scratch filled with ones, call {i}")
+        lay.workspace[n:].fill_(0xFF)
+        lay.step(zt, bt, po, sums=True)
+        check(lay.step_results(), want, w.K)
+
+
+@pytest.mark.parametrize("P", [1, 3])
+def test_layer_long_blocks_add_fine_counts_to_slabs(eqb, P):
+    """With more than 65,535 rows per block (a grid cap of 2) a block cannot
+    hold its fine counts in 16-bit LDS counters to its end: the fine pass adds
+    them to the partition slabs after each segment, as the separate calls
+    do, and the fine selection sums the slabs."""
+    w = W.WORKLOADS["skew64"].with_T(140001, P)
+    z, b, off = W.generate(w)
+    if P > 1:
+        off = np.array([0] + [int(w.T * f) for f in CUTS[P]] + [w.T], np.int64)
+    say(f"long blocks {w.T} rows, P={P}, grid cap 2")
+    want = O.run_layer(z, b, w.K, off, threads=8)
+    for got in run_twice(eqb, z, b, w.K, off, cap=2):
         check(got, want, w.K)

@@ -89,7 +89,7 @@ def test_noalloc_layer_rejects_a_layer_beyond_its_scratch(eqb):
     zt = torch.from_numpy(z.view(np.int16)).to(dev)
     bt = torch.from_numpy(b).to(dev)
     o = outputs(eqb, w.T, w.E, w.K, w.P, dev)
-    assert eqb.eqb_layer_workspace_size(w.E, w.P) > eqb.EQB_NOALLOC_SCRATCH_BYTES
+    assert eqb.eqb_layer_workspace_zero_bytes(w.E, w.P) > eqb.EQB_NOALLOC_SCRATCH_BYTES
     with pytest.raises(eqb.EqbError) as ex:
         eqb.eqb_layer_noalloc(zt, bt, w.K, o["idx"], o["score"], o["tau"], o["load"], o["q"], o["b_next"],
                               o["status"], [int(x) for x in off])
