@@ -196,6 +196,7 @@ def lei_leg(w, eqb, torch, lay, load, zt, part_off, stream, reps=10):
 
 
 STAGES = ("route_hist1", "select1", "margin_hist2", "select2_center")
+ROUTE_EVENT_EVERY = 5        # timed steps per pair of route-kernel events
 
 
 def make_events(torch, n, k=5):
@@ -350,7 +351,9 @@ def time_layer(eqb, torch, w, zt, bt, po, stream, steps, warmup, min_warmup_s, s
     between every kernel and host timestamps around every call."""
     lay = eqb.Layer(w.T, w.E, w.K, w.P, device=zt.device)
     lay._layer_buffers()
-    rev = make_events(torch, steps, 2)
+    # Route-kernel events on every ROUTE_EVENT_EVERY-th step of the timed
+    # region: each event record costs the queue a few microseconds.
+    rev = make_events(torch, (steps + ROUTE_EVENT_EVERY - 1) // ROUTE_EVENT_EVERY, 2)
     rmarks = [eqb.layer_marks([a, b, None, None, None]) for a, b in rev]
     sev = make_events(torch, stage_steps)
     smarks = [eqb.layer_marks(e) for e in sev]
@@ -369,10 +372,12 @@ def time_layer(eqb, torch, w, zt, bt, po, stream, steps, warmup, min_warmup_s, s
                 torch.cuda.synchronize()
         torch.cuda.synchronize()
         # Timed region: exactly `steps` layers; the only events in it are the
-        # two eqb_layer records around the route kernel on its own stream.
+        # two eqb_layer records around the route kernel on its own stream, on
+        # every ROUTE_EVENT_EVERY-th step.
         t0 = time.perf_counter()
         for i in range(steps):
-            lay.step(zt, bt, po, marks=rmarks[i], stream=stream)
+            m = rmarks[i // ROUTE_EVENT_EVERY] if i % ROUTE_EVENT_EVERY == 0 else None
+            lay.step(zt, bt, po, marks=m, stream=stream)
         torch.cuda.synchronize()
         elapsed = time.perf_counter() - t0
         # Stage breakdown: a separate run with an event after every kernel.
@@ -403,7 +408,8 @@ def time_layer(eqb, torch, w, zt, bt, po, stream, steps, warmup, min_warmup_s, s
                  "host_enqueue_ms": stats(host), "device_idle_between_steps_ms": stats(gaps),
                  "outliers": outliers, "steps": stage_steps,
                  "note": "a separate run with an event after every kernel (eqb_layer marks)"}
-    return lay, elapsed * 1e3 / steps, warmup_run, float(np.mean(route)), stats(route), breakdown
+    route_stats = dict(stats(route), launches=len(route), of_timed_steps=f"every {ROUTE_EVENT_EVERY}th")
+    return lay, elapsed * 1e3 / steps, warmup_run, float(np.mean(route)), route_stats, breakdown
 
 
 def bench_line(w, ms_per_step, warmup_args, route_ms, route_stats, breakdown):

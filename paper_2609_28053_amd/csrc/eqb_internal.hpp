@@ -41,12 +41,13 @@ struct MarginArgs {
 // byte j in their low and high halves.
 __host__ __device__ inline int64_t part_words(int E) { return (int64_t)(E / 2) * kNBins; }
 // Blocks of the fine pass per compute unit (its LDS counts take (E/2) * 257
-// words per block) and the per-block images a layer workspace holds: enough
-// for one full grid on a device of up to 256 compute units (a larger device
-// runs the pass with fewer, longer blocks).
+// words per block) when it adds its counts to slabs, and the per-block images
+// a layer workspace holds: the image-storing pass runs one block per compute
+// unit, and the workspace has room for one full grid on a device of up to
+// 256 compute units (a larger device runs the pass with fewer, longer blocks).
 inline int margin_blocks_per_cu(int E) { return (E / 2) * kHistStride * 4 * 2 <= 160 * 1024 ? 2 : 1; }
 constexpr int kPartCUs = 256;
-inline int layer_part_blocks(int E) { return kPartCUs * margin_blocks_per_cu(E); }
+inline int layer_part_blocks(int) { return kPartCUs; }
 
 eqb_status launch_route(const RouteArgs& a, hipStream_t s);
 // *part_used: the number of per-block images the fine pass wrote (0 when it

@@ -202,16 +202,14 @@ def test_layer_workspace_size(lib):
     # slabs per partition below 16 partitions, else 1), the [P,E] loads and
     # three [E] selections, each rounded up to 256 bytes, and 1,024 claim
     # counters of the route sweep's dynamic tails, 128 bytes apart.  Then the
-    # fine pass's per-block images, E/2 * 256 words each, for one or two
-    # blocks per compute unit (two when two blocks' LDS counts, (E/2) * 257
-    # words each, fit in 160 KiB) on 256 compute units.
+    # fine pass's per-block images, E/2 * 256 words each, for one block per
+    # compute unit on 256 compute units.
     for E, P in ((8, 1), (64, 4), (128, 3), (256, 1), (256, 16), (256, 17), (256, 256)):
         nsub = 1 if P >= 16 else 16 // P
         zero = (2 * P * nsub * E * 1024 + -(-4 * P * E // 256) * 256 + 2 * -(-4 * E // 256) * 256
                 + -(-8 * E // 256) * 256 + 1024 * 128)
-        blocks = 256 * (2 if (E // 2) * 257 * 4 * 2 <= 160 * 1024 else 1)
         assert lib.eqb_layer_workspace_zero_bytes(E, P) == zero
-        assert lib.eqb_layer_workspace_size(E, P) == zero + blocks * (E // 2) * 256 * 4
+        assert lib.eqb_layer_workspace_size(E, P) == zero + 256 * (E // 2) * 256 * 4
     assert lib.eqb_layer_workspace_size(256, 1) - lib.eqb_layer_workspace_zero_bytes(256, 1) == 32 << 20
     for E, P in ((12, 1), (8, 0), (8, 257)):
         assert lib.eqb_layer_workspace_size(E, P) == 0
