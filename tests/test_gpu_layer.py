@@ -7,6 +7,7 @@ summed); the rest is scratch for the fine pass's per-block count images.
 Every layer below runs twice on the same workspace: the second run can only
 match the oracle if the first left the counters zeroed.
 """
+import dataclasses
 import sys
 
 import numpy as np
@@ -167,3 +168,22 @@ def test_layer_long_blocks_add_fine_counts_to_slabs(eqb, P):
     want = O.run_layer(z, b, w.K, off, threads=8)
     for got in run_twice(eqb, z, b, w.K, off, cap=2):
         check(got, want, w.K)
+
+
+# Small layers of every expert count: a single row, a few rows (fewer than
+# one block step, so every block of the fine pass stores an image of almost
+# nothing), K up to E - 1 (the generic route kernel past K = 14), several
+# partitions.
+SMALL = [(8, 1, 1, 1), (8, 7, 17, 2), (16, 3, 1, 1), (16, 9, 2, 1), (16, 15, 4099, 3),
+         (32, 5, 3, 2), (32, 31, 1001, 3), (64, 1, 1, 1), (64, 14, 65, 4), (256, 255, 3, 1),
+         (256, 16, 777, 2)]
+
+
+@pytest.mark.parametrize("E,K,T,P", SMALL, ids=[f"E{c[0]}-K{c[1]}-T{c[2]}-P{c[3]}" for c in SMALL])
+def test_layer_small_shapes(eqb, E, K, T, P):
+    w = dataclasses.replace(W.WORKLOADS["skew64"], name=f"small{E}", E=E, K=K, T=T, P=P, seed=100 + E + K)
+    z, b, off = W.generate(w)
+    say(f"small layer E={E} K={K} T={T} P={P}")
+    want = O.run_layer(z, b, K, off, threads=8)
+    for got in run_twice(eqb, z, b, K, off):
+        check(got, want, K)
