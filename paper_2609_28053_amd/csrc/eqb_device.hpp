@@ -412,10 +412,15 @@ __device__ __forceinline__ void block_rows(int64_t T, int64_t rows_per_block, in
 // block's range it claims pool chunks from the group's counter until none is
 // left.  Groups keep the claims on one counter few.  Static ranges are
 // flushed every kSegPool rows, so a block's last static segment plus any pool
-// rows it takes stay below the 16-bit LDS counters' limit.
-constexpr int64_t kPoolMax = 32768;
-constexpr int64_t kPoolDiv = 8;
-constexpr int kGroupBlocks = 16;
+// rows it takes stay below the 16-bit LDS counters' limit.  Groups of 8 with
+// half their rows pooled (at most 49,152: a large workload's group of 8 keeps
+// 37.5% back and its blocks' 10,240-row static ranges stay one segment)
+// measured 2-3.5% faster per step than groups of 16 pooling an eighth
+// (4,194,304 tokens), and 1-2% at 1.5-2 M tokens; groups of 4, and pools of
+// a quarter or a third, fell in between.
+constexpr int64_t kPoolMax = 49152;
+constexpr int64_t kPoolDiv = 2;
+constexpr int kGroupBlocks = 8;
 constexpr int64_t kSegPool = kSegMax - kPoolMax;
 // A group's claim counter is indexed by the group's first block and sits on
 // its own 128-byte line; pool mode is used for grids of at most

@@ -113,7 +113,7 @@ def test_layer_equals_the_call_sequence(eqb):
 # The one-call layer's route sweep takes its last rows as dynamic tails
 # (chunks that each block's waves claim once their own range is done) when a
 # block's range is long; a grid cap makes the ranges long at sizes the oracle
-# finishes quickly.  Groups of up to 16 blocks per partition, one or several
+# finishes quickly.  Groups of up to 8 blocks per partition, one or several
 # groups, partitions of unequal size and the hard rows (dry lanes, ties,
 # equal logits) of the routing tests.
 DYNAMIC = [("large256", 131072, 1, 16), ("large256", 262144, 1, 40), ("large256", 196608, 5, 24),
