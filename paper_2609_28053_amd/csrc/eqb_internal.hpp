@@ -88,11 +88,14 @@ eqb_status launch_lei_router_backward(const uint16_t* z, const int32_t* idx, con
 eqb_status launch_lei_inject(float* grad, const float* inj, int64_t T, int E, const PartTable& pt,
                              hipStream_t s);
 
-// Count slabs per partition in a layer's workspace: enough that about 16
-// slabs share the blocks of a launch (a partition of the large workload's
-// 16 already has its own), so no counter receives the flush atomics of
-// every block.
-inline int layer_replicas(int P) { return P >= 16 ? 1 : 16 / P; }
+// Count slabs per partition in a layer's workspace: enough that about 8
+// slabs share the blocks of a launch, so no counter receives the flush
+// atomics of every block.  Only the route sweep's coarse counts use them
+// when the fine pass stores per-block images, and the coarse selection reads
+// and clears every slab: 8 measured faster than 16, 4, 2 or 1 at one
+// partition of 147,456 tokens (1.2% against 16), and no slower on the other
+// workloads.
+inline int layer_replicas(int P) { return P >= 8 ? 1 : 8 / P; }
 
 // Working buffers of one layer (eqb_layer): the per-partition coarse and
 // fine counts (layer_replicas(P) slabs per partition), the loads as the

@@ -198,14 +198,14 @@ def layer(lib, T=64, E=8, K=2, ws=ctypes.c_void_p(0x10000), ws_bytes=1 << 30, po
 
 
 def test_layer_workspace_size(lib):
-    # Counters: two sets of [P,nsub,E,256] int32 count slabs (nsub = 16 // P
-    # slabs per partition below 16 partitions, else 1), the [P,E] loads and
+    # Counters: two sets of [P,nsub,E,256] int32 count slabs (nsub = 8 // P
+    # slabs per partition below 8 partitions, else 1), the [P,E] loads and
     # three [E] selections, each rounded up to 256 bytes, and 1,024 claim
     # counters of the route sweep's dynamic tails, 128 bytes apart.  Then the
     # fine pass's per-block images, E/2 * 256 words each, for one block per
     # compute unit on 256 compute units.
     for E, P in ((8, 1), (64, 4), (128, 3), (256, 1), (256, 16), (256, 17), (256, 256)):
-        nsub = 1 if P >= 16 else 16 // P
+        nsub = 1 if P >= 8 else 8 // P
         zero = (2 * P * nsub * E * 1024 + -(-4 * P * E // 256) * 256 + 2 * -(-4 * E // 256) * 256
                 + -(-8 * E // 256) * 256 + 1024 * 128)
         assert lib.eqb_layer_workspace_zero_bytes(E, P) == zero
