@@ -7,7 +7,9 @@
 // issued before a step is counted.  Margins are rounded to BF16 two at a time
 // by the hardware conversion (round to nearest even, subnormals kept).  Counts
 // go to packed LDS histograms indexed by the raw BF16 byte; the flush maps
-// them to kappa bins.
+// them to kappa bins.  In the one-call layer the fine pass instead stores
+// each block's LDS counts, raw bytes and all, as one image that the fine
+// selection sums (select.hip).
 #include "eqb_internal.hpp"
 
 namespace eqb {
