@@ -28,6 +28,11 @@ struct PartTable {
   // Claim counters of the partitions' dynamic tails (one int32 per
   // partition, 256 bytes apart, zero at launch), or null: see block_plan.
   int32_t* pool = nullptr;
+  // Coarse count slabs of 16-bit counters (the layer's route sweep, where no
+  // slab can receive more than 65,535 rows): slab [E/2][256][2], the counters
+  // of experts 2m and 2m+1 for kappa bin k side by side at (m*256 + k)*2,
+  // in the first half of the slab's int32 space.
+  int32_t slab16 = 0;
 };
 
 // The [E,256] count slab that this block adds partition p's counts to: with

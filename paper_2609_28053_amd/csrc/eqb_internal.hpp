@@ -16,6 +16,9 @@ struct RouteArgs {
   int32_t* load;
   int32_t* hist;
   PartTable pt;
+  // The layer: `hist` is workspace slabs that only its own coarse selection
+  // reads, so the route kernel may use 16-bit counters (PartTable::slab16).
+  bool slab16_ok = false;
 };
 
 struct MarginArgs {
@@ -49,7 +52,8 @@ inline int margin_blocks_per_cu(int E) { return (E / 2) * kHistStride * 4 * 2 <=
 constexpr int kPartCUs = 256;
 inline int layer_part_blocks(int) { return kPartCUs; }
 
-eqb_status launch_route(const RouteArgs& a, hipStream_t s);
+// *slab16_used: the coarse counts went to 16-bit slabs (see PartTable).
+eqb_status launch_route(const RouteArgs& a, hipStream_t s, bool* slab16_used = nullptr);
 // *part_used: the number of per-block images the fine pass wrote (0 when it
 // added its counts to a.hist).
 eqb_status launch_margin(bool fine, const MarginArgs& a, hipStream_t s, int* part_used = nullptr);
@@ -59,10 +63,11 @@ eqb_status launch_select(int pass, const int32_t* hist, int P, int E, int64_t r,
                          int64_t* rank_in_bin, int32_t* sel_lo, uint16_t* q_bf16, float* b_next,
                          int32_t* hist_sum, int32_t* status, hipStream_t s);
 
+// slab16: the pass-1 slabs hold 16-bit counters (PartTable::slab16).
 eqb_status launch_layer_selects(int pass, int32_t* hist, int P, int nsub, int E, int64_t r, int32_t* sel_hi,
                                 int64_t* rank_in_bin, int32_t* sel_lo, uint16_t* q_bf16, float* b_next,
                                 int32_t* hist_sum, int32_t* load_acc, int32_t* load_out, int32_t* status,
-                                int32_t* pool_reset, hipStream_t s);
+                                int32_t* pool_reset, hipStream_t s, bool slab16 = false);
 // The fine selection of a layer from the fine pass's per-block images
 // (nparts of them), then the centring and status as launch_layer_selects(2).
 eqb_status launch_layer_select_parts(const uint32_t* part, int nparts, int E, int32_t* sel_hi,
@@ -221,6 +226,26 @@ inline PartTable pool_table(const PartTable& pt, int64_t T, int blocks, int64_t 
     }
   }
   return out;
+}
+
+// Most rows any count slab of a route launch with static ranges receives:
+// block b covers rows [b * rows_per_block, (b + 1) * rows_per_block) and adds
+// partition p's rows to slab p * nsub + b % nsub, so a slab of partition p
+// takes at most ceil(c_p / nsub) blocks' rows, c_p the blocks overlapping p.
+inline int64_t slab_rows_bound(const PartTable& pt, int64_t T, int blocks, int64_t rows_per_block) {
+  (void)blocks;
+  int64_t worst = 0;
+  for (int p = 0; p < pt.P; ++p) {
+    if (pt.off[p + 1] <= pt.off[p]) continue;
+    const int64_t b0 = pt.off[p] / rows_per_block, b1 = (pt.off[p + 1] - 1) / rows_per_block;
+    const int64_t c = b1 - b0 + 1;
+    const int64_t per = (c + pt.nsub - 1) / pt.nsub;
+    const int64_t n = pt.off[p + 1] - pt.off[p];
+    const int64_t rows = per * rows_per_block < n ? per * rows_per_block : n;
+    worst = rows > worst ? rows : worst;
+  }
+  (void)T;
+  return worst;
 }
 
 }  // namespace eqb

@@ -115,6 +115,35 @@ __device__ __forceinline__ void flush_hist_slots(uint32_t* sh, int32_t* __restri
   }
 }
 
+// flush_hist_slots into a slab of 16-bit counters (PartTable::slab16): an LDS
+// word already holds the counts of experts e and e+1 (e = 4j + 2h) for one raw
+// bin, so the item's two words (raw bins 2b, 2b+1, kappa bins k, k+1 or k, k-1)
+// are four adjacent 16-bit counters of the slab, added with one 64-bit atomic.
+// The host uses it only where no counter can pass 65,535 (no carry between
+// the fields).
+template <int E>
+__device__ __forceinline__ void flush_hist_slots16(uint32_t* sh, int32_t* __restrict__ slab32) {
+  constexpr int kItems = fast_hist_words<E>() / 2;
+  uint16_t* slab = reinterpret_cast<uint16_t*>(slab32);
+  for (int i = threadIdx.x; i < kItems; i += blockDim.x) {
+    const int it = flush_word(i, kItems);
+    const int arr = it >> 13, j = (it >> 6) & 127, slot = it & 63;
+    const int w0 = arr * 16384 + 2 * j * 64 + slot;
+    const uint32_t c0 = sh[w0], c1 = sh[w0 + 64];
+    if (c0 | c1) {
+      const int m = 2 * (63 - slot) + arr;   // the pair of experts 2m, 2m+1
+      const bool neg = (2 * j) & 0x80;
+      const int k0 = kappa_hi_of_raw(2 * j);  // even, or odd (flipped) for negative bins
+      const int k = neg ? k0 - 1 : k0;
+      const uint64_t v = neg ? ((uint64_t)c1 | ((uint64_t)c0 << 32)) : ((uint64_t)c0 | ((uint64_t)c1 << 32));
+      atomicAdd(reinterpret_cast<unsigned long long*>(slab + ((int64_t)m * kNBins + k) * 2),
+                (unsigned long long)v);
+      sh[w0] = 0;
+      sh[w0 + 64] = 0;
+    }
+  }
+}
+
 // The histogram byte offset of half 1 of a piece: byte 3 of its index bytes
 // to byte 0, 1 to byte 2.  Volatile so that it is formed where it is used
 // rather than kept in a register per piece.
@@ -682,8 +711,12 @@ __global__ __launch_bounds__(kRouteBlock) void route_fast_kernel(
   auto flush_counts = [&](int p) {
     __syncthreads();
     if (hist) {
-      if constexpr (kSlotHist<E>) flush_hist_slots<E>(sh_hist, count_slab(hist, pt, p, E));
-      else flush_hist<E, false>(sh_hist, count_slab(hist, pt, p, E), nullptr);
+      if constexpr (kSlotHist<E>) {
+        if (pt.slab16) flush_hist_slots16<E>(sh_hist, count_slab(hist, pt, p, E));
+        else flush_hist_slots<E>(sh_hist, count_slab(hist, pt, p, E));
+      } else {
+        flush_hist<E, false>(sh_hist, count_slab(hist, pt, p, E), nullptr);
+      }
     }
     if (load) {
       for (int e = threadIdx.x; e < E; e += kRouteBlock) {
@@ -854,30 +887,34 @@ __global__ __launch_bounds__(kBlock) void route_generic_kernel(
 constexpr int64_t kPoolMinSteps = 64;
 
 template <int E, int KT>
-void launch_fast(const RouteArgs& a, hipStream_t s) {
+void launch_fast(const RouteArgs& a, hipStream_t s, bool* slab16_used) {
   int blocks;
   int64_t rpb;
   grid_for(a.T, kRouteWaves * (64 / FastCfg<E>::G), 1, &blocks, &rpb);
+  PartTable pt = pool_table(a.pt, a.T, blocks, kPoolMinSteps * kRouteWaves * (64 / FastCfg<E>::G));
+  pt.slab16 = (kSlotHist<E> && a.hist != nullptr && a.slab16_ok && pt.pool == nullptr &&
+               slab_rows_bound(pt, a.T, blocks, rpb) <= kSegMax) ? 1 : 0;
+  if (slab16_used) *slab16_used = pt.slab16 != 0;
   route_fast_kernel<E, KT><<<blocks, kRouteBlock, 0, s>>>(a.z, a.b, a.T, a.K, a.idx, a.score, a.tau, a.load,
-                                                     a.hist, pool_table(a.pt, a.T, blocks, kPoolMinSteps * kRouteWaves * (64 / FastCfg<E>::G)),
-                                                     rpb);
+                                                     a.hist, pt, rpb);
 }
 
 template <int E>
-eqb_status launch_route_e(const RouteArgs& a, hipStream_t s) {
+eqb_status launch_route_e(const RouteArgs& a, hipStream_t s, bool* slab16_used) {
+  if (slab16_used) *slab16_used = false;
   if (a.K <= kFastKmax) {
     // the common MoE fan-outs get a kernel with the rounds unrolled
     if constexpr (E >= 64) {
       switch (a.K) {
-        case 1: launch_fast<E, 1>(a, s); return launch_status();
-        case 2: launch_fast<E, 2>(a, s); return launch_status();
-        case 4: launch_fast<E, 4>(a, s); return launch_status();
-        case 6: launch_fast<E, 6>(a, s); return launch_status();
-        case 8: launch_fast<E, 8>(a, s); return launch_status();
+        case 1: launch_fast<E, 1>(a, s, slab16_used); return launch_status();
+        case 2: launch_fast<E, 2>(a, s, slab16_used); return launch_status();
+        case 4: launch_fast<E, 4>(a, s, slab16_used); return launch_status();
+        case 6: launch_fast<E, 6>(a, s, slab16_used); return launch_status();
+        case 8: launch_fast<E, 8>(a, s, slab16_used); return launch_status();
         default: break;
       }
     }
-    launch_fast<E, 0>(a, s);
+    launch_fast<E, 0>(a, s, slab16_used);
   } else {
     int blocks;
     int64_t rpb;
@@ -890,14 +927,14 @@ eqb_status launch_route_e(const RouteArgs& a, hipStream_t s) {
   return launch_status();
 }
 
-eqb_status launch_route(const RouteArgs& a, hipStream_t s) {
+eqb_status launch_route(const RouteArgs& a, hipStream_t s, bool* slab16_used) {
   switch (a.E) {
-    case 8: return launch_route_e<8>(a, s);
-    case 16: return launch_route_e<16>(a, s);
-    case 32: return launch_route_e<32>(a, s);
-    case 64: return launch_route_e<64>(a, s);
-    case 128: return launch_route_e<128>(a, s);
-    case 256: return launch_route_e<256>(a, s);
+    case 8: return launch_route_e<8>(a, s, slab16_used);
+    case 16: return launch_route_e<16>(a, s, slab16_used);
+    case 32: return launch_route_e<32>(a, s, slab16_used);
+    case 64: return launch_route_e<64>(a, s, slab16_used);
+    case 128: return launch_route_e<128>(a, s, slab16_used);
+    case 256: return launch_route_e<256>(a, s, slab16_used);
     default: return EQB_ERR_UNSUPPORTED;
   }
 }

@@ -15,7 +15,9 @@ namespace eqb {
 // the loads accumulated by the route kernel (load_acc [P,E]) are copied to
 // load_out and zeroed, so the workspace is left as it was found: all zero.
 // Each counter is read and cleared by the same thread.
-template <bool kLocal>
+// kSlab16 (the layer, global form): the P slabs hold 16-bit counters in the
+// layout of PartTable::slab16; each is read, summed and cleared as a uint16.
+template <bool kLocal, bool kSlab16 = false>
 __global__ __launch_bounds__(kNBins) void select_coarse_kernel(
     int32_t* __restrict__ hist, int P, int E, int K, int64_t r, const PartTable pt,
     int32_t* __restrict__ sel_hi, int64_t* __restrict__ rank_in_bin, int32_t* __restrict__ hist_sum,
@@ -42,9 +44,25 @@ __global__ __launch_bounds__(kNBins) void select_coarse_kernel(
   if (kLocal) {
     c = hist[((int64_t)p * E + e) * kNBins + u];
   } else {
-    c = slab_sum(hist + (int64_t)e * kNBins + u, P, (int64_t)E * kNBins);
+    if (kSlab16) {
+      uint16_t* h16 = reinterpret_cast<uint16_t*>(hist) + ((int64_t)(e >> 1) * kNBins + u) * 2 + (e & 1);
+      const int64_t stride = (int64_t)E * kNBins * 2;  // one int32 slab, in 16-bit units
+      int q = 0;
+      for (; q + 8 <= P; q += 8) {
+        uint32_t v[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) v[j] = h16[(q + j) * stride];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) c += v[j];
+      }
+      for (; q < P; ++q) c += h16[q * stride];
+      if (clear)
+        for (int q2 = 0; q2 < P; ++q2) h16[q2 * stride] = 0;
+    } else {
+      c = slab_sum(hist + (int64_t)e * kNBins + u, P, (int64_t)E * kNBins);
+      if (clear) slab_clear(hist + (int64_t)e * kNBins + u, P, (int64_t)E * kNBins);
+    }
     if (hist_sum) hist_sum[(int64_t)e * kNBins + u] = (int32_t)c;
-    if (clear) slab_clear(hist + (int64_t)e * kNBins + u, P, (int64_t)E * kNBins);
     if (load_acc) {
       for (int q = u; q < pt.P; q += kNBins) {
         load_out[(int64_t)q * E + e] = load_acc[(int64_t)q * E + e];
@@ -233,13 +251,17 @@ __global__ __launch_bounds__(256) void center_kernel(const uint16_t* __restrict_
 eqb_status launch_layer_selects(int pass, int32_t* hist, int P, int nsub, int E, int64_t r, int32_t* sel_hi,
                                 int64_t* rank_in_bin, int32_t* sel_lo, uint16_t* q_bf16, float* b_next,
                                 int32_t* hist_sum, int32_t* load_acc, int32_t* load_out, int32_t* status,
-                                int32_t* pool_reset, hipStream_t s) {
+                                int32_t* pool_reset, hipStream_t s, bool slab16) {
   PartTable none{};
   none.P = P;
   const int nslabs = P * nsub;
   if (pass == 1) {
-    select_coarse_kernel<false><<<E, kNBins, 0, s>>>(hist, nslabs, E, 0, r, none, sel_hi, rank_in_bin, hist_sum,
-                                                     nullptr, true, load_acc, load_out, pool_reset);
+    if (slab16)
+      select_coarse_kernel<false, true><<<E, kNBins, 0, s>>>(hist, nslabs, E, 0, r, none, sel_hi, rank_in_bin,
+                                                             hist_sum, nullptr, true, load_acc, load_out, pool_reset);
+    else
+      select_coarse_kernel<false><<<E, kNBins, 0, s>>>(hist, nslabs, E, 0, r, none, sel_hi, rank_in_bin, hist_sum,
+                                                       nullptr, true, load_acc, load_out, pool_reset);
     return launch_status();
   }
   select_fine_kernel<false><<<E, kNBins, 0, s>>>(hist, nslabs, E, none, sel_hi, rank_in_bin, sel_lo, q_bf16,
@@ -272,14 +294,16 @@ eqb_status launch_layer(const RouteArgs& route, int64_t r, const LayerWorkspace&
   a.hist = w.hist_hi;
   a.pt.nsub = w.nsub;
   a.pt.pool = w.pool;
+  a.slab16_ok = true;
   eqb_status st = mark(marks, 0, s);
   if (st != EQB_OK) return st;
-  st = launch_route(a, s);
+  bool slab16 = false;
+  st = launch_route(a, s, &slab16);
   if (st != EQB_OK) return st;
   if ((st = mark(marks, 1, s)) != EQB_OK) return st;
   const int P = a.pt.P, E = a.E;
   st = launch_layer_selects(1, w.hist_hi, P, w.nsub, E, r, w.sel_hi, w.rank_in_bin, nullptr, nullptr, nullptr,
-                            hist_hi_sum, w.load_acc, load_out, nullptr, w.pool, s);
+                            hist_hi_sum, w.load_acc, load_out, nullptr, w.pool, s, slab16);
   if (st != EQB_OK) return st;
   if ((st = mark(marks, 2, s)) != EQB_OK) return st;
   MarginArgs m;

@@ -170,6 +170,30 @@ def test_layer_long_blocks_add_fine_counts_to_slabs(eqb, P):
         check(got, want, w.K)
 
 
+# The layer's route sweep adds its coarse counts to 16-bit slab counters where
+# no slab can take more than 65,535 rows.  A grid cap of 96 gives 12 blocks per
+# slab (8 slabs per partition at P = 1, 4 at P = 2) and no dynamic tails; with
+# 5,461 rows per block a slab takes 65,532 rows (16-bit counters), with 5,462
+# it takes 65,544 (the 32-bit form).  Every column is one value, so each
+# expert's rows all land in one bin and that counter reaches its bound.
+LIMIT = [(5461, 1), (5462, 1), (5461, 2), (5462, 2)]
+
+
+@pytest.mark.parametrize("rpb,P", LIMIT, ids=[f"rows{c[0]}-P{c[1]}" for c in LIMIT])
+def test_layer_coarse_counts_at_the_16bit_bound(eqb, rpb, P):
+    T, E, K = 96 * rpb, 64, 4
+    rng = np.random.default_rng(rpb + P)
+    col = W._to_bf16_bits(rng.normal(0.0, 1.0, E).astype(np.float32))
+    z = np.broadcast_to(col, (T, E)).copy()
+    b = np.zeros(E, np.float32)
+    off = None if P == 1 else np.array([0, T // 2, T], np.int64)
+    say(f"one value per column, T={T} E={E} K={K} P={P}, grid cap 96")
+    want = O.run_layer(z, b, K, off, threads=8)
+    assert want["H"].max() == T
+    for got in run_twice(eqb, z, b, K, off, cap=96):
+        check(got, want, K)
+
+
 # Small layers of every expert count: a single row, a few rows (fewer than
 # one block step, so every block of the fine pass stores an image of almost
 # nothing), K up to E - 1 (the generic route kernel past K = 14), several
