@@ -232,8 +232,7 @@ inline PartTable pool_table(const PartTable& pt, int64_t T, int blocks, int64_t 
 // block b covers rows [b * rows_per_block, (b + 1) * rows_per_block) and adds
 // partition p's rows to slab p * nsub + b % nsub, so a slab of partition p
 // takes at most ceil(c_p / nsub) blocks' rows, c_p the blocks overlapping p.
-inline int64_t slab_rows_bound(const PartTable& pt, int64_t T, int blocks, int64_t rows_per_block) {
-  (void)blocks;
+inline int64_t slab_rows_bound(const PartTable& pt, int64_t rows_per_block) {
   int64_t worst = 0;
   for (int p = 0; p < pt.P; ++p) {
     if (pt.off[p + 1] <= pt.off[p]) continue;
@@ -244,7 +243,6 @@ inline int64_t slab_rows_bound(const PartTable& pt, int64_t T, int blocks, int64
     const int64_t rows = per * rows_per_block < n ? per * rows_per_block : n;
     worst = rows > worst ? rows : worst;
   }
-  (void)T;
   return worst;
 }
 

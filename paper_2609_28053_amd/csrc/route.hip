@@ -893,7 +893,7 @@ void launch_fast(const RouteArgs& a, hipStream_t s, bool* slab16_used) {
   grid_for(a.T, kRouteWaves * (64 / FastCfg<E>::G), 1, &blocks, &rpb);
   PartTable pt = pool_table(a.pt, a.T, blocks, kPoolMinSteps * kRouteWaves * (64 / FastCfg<E>::G));
   pt.slab16 = (kSlotHist<E> && a.hist != nullptr && a.slab16_ok && pt.pool == nullptr &&
-               slab_rows_bound(pt, a.T, blocks, rpb) <= kSegMax) ? 1 : 0;
+               slab_rows_bound(pt, rpb) <= kSegMax) ? 1 : 0;
   if (slab16_used) *slab16_used = pt.slab16 != 0;
   route_fast_kernel<E, KT><<<blocks, kRouteBlock, 0, s>>>(a.z, a.b, a.T, a.K, a.idx, a.score, a.tau, a.load,
                                                      a.hist, pt, rpb);

@@ -194,6 +194,22 @@ def test_layer_coarse_counts_at_the_16bit_bound(eqb, rpb, P):
         check(got, want, K)
 
 
+@pytest.mark.parametrize("P", [1, 3])
+def test_layer_runs_of_equal_rows(eqb, P):
+    """A run of 1,500 equal rows puts a few blocks' rows into one fine bin of
+    some experts: those blocks' images hold counts far above the others'."""
+    w = W.WORKLOADS["skew64"].with_T(40000, P)
+    z, b, off = W.generate(w)
+    z[10000:11500] = z[10000]
+    if P > 1:
+        off = np.array([0] + [int(w.T * f) for f in CUTS[P]] + [w.T], np.int64)
+    say(f"run of equal rows, T={w.T} P={P}")
+    want = O.run_layer(z, b, w.K, off, threads=8)
+    assert want["L"].max() >= 1500   # the run lands in one fine bin of some expert
+    for got in run_twice(eqb, z, b, w.K, off):
+        check(got, want, w.K)
+
+
 # Small layers of every expert count: a single row, a few rows (fewer than
 # one block step, so every block of the fine pass stores an image of almost
 # nothing), K up to E - 1 (the generic route kernel past K = 14), several
