@@ -15,6 +15,7 @@ import torch
 
 import workloads as W
 from oracle import eqb_oracle as O
+from random_layers import random_layer_case
 
 pytestmark = pytest.mark.gpu
 
@@ -535,3 +536,20 @@ def test_common_bias_shift_on_gpu(eqb):
     qc = (c["bhat"].astype(np.uint32) << 16).view(np.float32)
     np.testing.assert_array_equal(qc, qa + np.float32(0.25))
     np.testing.assert_array_equal(c["b_next"], a["b_next"])
+
+
+# ------------------------------------------------------ random shapes -----
+@pytest.mark.parametrize("i", range(24))
+def test_random_shapes_calls(eqb, i):
+    """The separate calls (fused pass 1 and the standalone pass-1 kernel) on
+    the seeded random layers of the one-call layer's test, per-partition
+    counts included, under each case's grid cap."""
+    w, z, b, off, cap = random_layer_case(i)
+    say(f"random calls {i}: T={w.T} E={w.E} K={w.K} P={w.P} kind={w.kind} cuts={off.tolist()} cap={cap}")
+    want = O.run_layer(z, b, w.K, off, threads=_threads())
+    try:
+        eqb.eqb_set_max_blocks(cap)
+        for fused in (True, False):
+            assert_parity(gpu_layer(eqb, z, b, w.K, off, fused=fused), want, w.K)
+    finally:
+        eqb.eqb_set_max_blocks(0)
