@@ -239,3 +239,47 @@ def test_layer_random_shapes(eqb, i):
     want = O.run_layer(z, b, w.K, off, threads=8)
     for got in run_twice(eqb, z, b, w.K, off, cap=cap):
         check(got, want, w.K)
+
+
+@pytest.mark.parametrize("P", [1, 4])
+def test_layer_beyond_4gib_of_logits(eqb, P):
+    """131 copies of a 65,536-token batch (E = 256): 8,585,216 tokens and
+    4.4 GB of logits, so offsets into z pass 2^32 bytes (dynamic tails and
+    per-block fine images at that size).  Each row's routing is its copy's,
+    every count is 131 times the copy's (a partition's loads: its copies
+    times the copy's), and the r-th largest key of 131 copies, r = 131 r_M, is
+    the r_M-th of one copy: the quantile and the centred bias are the copy's,
+    which the oracle gives on one copy."""
+    M, n = 65536, 131
+    w = W.WORKLOADS["large256"].with_T(M, 1)
+    z, b, _ = W.generate(w)
+    want = O.run_layer(z, b, w.K, None, threads=8)
+    T, K = n * M, w.K
+    copies = {1: [n], 4: [17, 43, 1, 70]}[P]
+    off = np.concatenate([[0], np.cumsum(copies) * M]).astype(np.int64)
+    say(f"{n} copies of {M} tokens, T={T} P={P}")
+    zt = torch.from_numpy(z.view(np.int16)).cuda().repeat(n, 1)
+    assert zt.numel() * 2 > 2 ** 32
+    bt = torch.from_numpy(b).cuda()
+    po = eqb.PartOffsets([int(x) for x in off])
+    lay = eqb.Layer(T, w.E, K, P)
+    want_idx = torch.from_numpy(np.ascontiguousarray(want["idx"], np.int32)).cuda()
+    want_tau = torch.from_numpy(want["tau"].view(np.int32)).cuda()
+    for _ in range(2):
+        lay.step(zt, bt, po, sums=True)
+        torch.cuda.synchronize()
+        assert int(lay.status.item()) == 0 and lay.counters_zero()
+        assert torch.equal(lay.topk_idx.view(n, M, K), want_idx.expand(n, M, K))
+        assert torch.equal(lay.tau.view(torch.int32).view(n, M), want_tau.expand(n, M))
+        score = lay.topk_score.view(n, M, K)
+        assert torch.equal(score, score[:1].expand(n, M, K))
+        ws = want["score"].astype(np.float64)
+        assert np.all(np.abs(score[0].cpu().numpy() - ws) <= SCORE_RTOL * np.abs(ws))
+        load = lay.load_out.cpu().numpy()
+        np.testing.assert_array_equal(load, np.array(copies)[:, None] * want["load"][0][None, :])
+        np.testing.assert_array_equal(lay.H.cpu().numpy(), n * want["H"])
+        np.testing.assert_array_equal(lay.L.cpu().numpy(), n * want["L"])
+        np.testing.assert_array_equal(lay.q_bf16.cpu().numpy().view(np.uint16), want["bhat"])
+        np.testing.assert_array_equal(lay.b_next.cpu().numpy().view(np.uint32), want["b_next"].view(np.uint32))
+    del zt
+    torch.cuda.empty_cache()
