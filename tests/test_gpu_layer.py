@@ -249,7 +249,7 @@ def test_layer_beyond_4gib_of_logits(eqb, P):
     every count is 131 times the copy's (a partition's loads: its copies
     times the copy's), and the r-th largest key of 131 copies, r = 131 r_M, is
     the r_M-th of one copy: the quantile and the centred bias are the copy's,
-    which the oracle gives on one copy."""
+    which the oracle gives on one copy.  The same for the separate calls."""
     M, n = 65536, 131
     w = W.WORKLOADS["large256"].with_T(M, 1)
     z, b, _ = W.generate(w)
@@ -281,5 +281,22 @@ def test_layer_beyond_4gib_of_logits(eqb, P):
         np.testing.assert_array_equal(lay.L.cpu().numpy(), n * want["L"])
         np.testing.assert_array_equal(lay.q_bf16.cpu().numpy().view(np.uint16), want["bhat"])
         np.testing.assert_array_equal(lay.b_next.cpu().numpy().view(np.uint32), want["b_next"].view(np.uint32))
+    del lay
+    # the separate calls on the same logits: per-partition counts are the
+    # partition's copies times the copy's
+    c = np.array(copies)[:, None, None]
+    for fused in (True, False):
+        say(f"separate calls, fused={fused}")
+        sep = eqb.run_layer(zt, bt, K, [int(x) for x in off], fused=fused)
+        torch.cuda.synchronize()
+        assert int(sep.dev_status.item()) == 0
+        assert torch.equal(sep.topk_idx.view(n, M, K), want_idx.expand(n, M, K))
+        assert torch.equal(sep.tau.view(torch.int32).view(n, M), want_tau.expand(n, M))
+        np.testing.assert_array_equal(sep.load.cpu().numpy(), c[:, :, 0] * want["load"][0][None, :])
+        np.testing.assert_array_equal(sep.hist_hi.cpu().numpy(), c * want["H_p"][0][None])
+        np.testing.assert_array_equal(sep.hist_lo.cpu().numpy(), c * want["L_p"][0][None])
+        np.testing.assert_array_equal(sep.q_bf16.cpu().numpy().view(np.uint16), want["bhat"])
+        np.testing.assert_array_equal(sep.b_next.cpu().numpy().view(np.uint32), want["b_next"].view(np.uint32))
+        del sep
     del zt
     torch.cuda.empty_cache()
