@@ -482,7 +482,7 @@ def main():
         return
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU: this build has no multi-GPU path "
+        print("bench.py measures one GPU: the library has no multi-GPU path "
               "(the per-rank all-reduce of Algorithm 1 is reproduced as a sum of partition "
               "histograms on one device). Run with --gpus 1.", file=sys.stderr)
         sys.exit(2)
