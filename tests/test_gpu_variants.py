@@ -10,6 +10,7 @@ import torch
 
 import workloads as W
 from oracle import balance_oracle as B
+from random_layers import random_layer_case
 
 pytestmark = pytest.mark.gpu
 
@@ -67,3 +68,34 @@ def test_histogram_qb_matches_oracle(eqb, name, T, P, lo, hi, nbins):
     np.testing.assert_array_equal(got["counts"], want_c)
     np.testing.assert_array_equal(got["est"].view(np.uint64), want_est.view(np.uint64))
     np.testing.assert_array_equal(got["b_next"].view(np.uint32), want_b.view(np.uint32))
+
+
+# The seeded random layers of the layer tests (every expert count, K up to
+# E - 1, unequal partitions with empty ones, grid caps, every data kind), with
+# a random histogram range and bin count for the fixed-resolution estimate.
+@pytest.mark.parametrize("i", range(16))
+def test_variants_on_random_shapes(eqb, i):
+    w, z, b, off, cap = random_layer_case(i)
+    rng = np.random.default_rng(9000 + i)
+    lo = float(np.float32(rng.uniform(-10.0, 0.0)))
+    hi = float(np.float32(lo + rng.uniform(0.5, 16.0)))
+    nbins = int(rng.integers(1, 257))
+    say(f"variants random {i}: T={w.T} E={w.E} K={w.K} cuts={off.tolist()} cap={cap} "
+        f"[{lo},{hi}) nbins={nbins}")
+    want_bp, want_avg, want_b = B.rank_averaged_qb(z, b, w.K, off)
+    want_c, want_est, want_hb = B.histogram_qb(z, b, w.K, off, lo, hi, nbins)
+    zt, bt = dev(z, b)
+    offl = [int(x) for x in off]
+    try:
+        eqb.eqb_set_max_blocks(cap)
+        got = eqb.rank_averaged_qb(zt, bt, w.K, offl)
+        hist = eqb.histogram_qb(zt, bt, w.K, lo, hi, nbins, offl)
+    finally:
+        eqb.eqb_set_max_blocks(0)
+    assert got["dev_status"] == 0 and hist["dev_status"] == 0
+    np.testing.assert_array_equal(got["bhat_p"], want_bp)
+    np.testing.assert_array_equal(got["b_avg"].view(np.uint64), want_avg.view(np.uint64))
+    np.testing.assert_array_equal(got["b_next"].view(np.uint32), want_b.view(np.uint32))
+    np.testing.assert_array_equal(hist["counts"], want_c)
+    np.testing.assert_array_equal(hist["est"].view(np.uint64), want_est.view(np.uint64))
+    np.testing.assert_array_equal(hist["b_next"].view(np.uint32), want_hb.view(np.uint32))
