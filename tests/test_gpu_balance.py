@@ -8,6 +8,7 @@ import torch
 
 import workloads as W
 from oracle import balance_oracle as B
+from random_layers import random_layer_case
 
 pytestmark = pytest.mark.gpu
 
@@ -76,6 +77,24 @@ def test_qb_loop_matches_oracle(eqb, name, T, P, steps):
     want = B.qb_loop(batches, b0, w.K, off, threads=8)
     zs = [torch.from_numpy(z.view(np.int16)).cuda() for z in batches]
     got = eqb.qb_loop(zs, torch.from_numpy(b0), w.K, [int(x) for x in off])
+    check_loop(got, want)
+
+
+@pytest.mark.parametrize("i", range(12))
+def test_qb_loop_on_random_shapes(eqb, i):
+    """Three steps of the closed loop on the seeded random layers of the layer
+    tests (fresh batches from the same distribution), under each case's grid
+    cap: every step's bias, loads, MaxVio and next bias against the oracle."""
+    w, _, b0, off, cap = random_layer_case(i)
+    batches = [W.generate(w, batch=q)[0] for q in range(3)]
+    say(f"qb loop random {i}: T={w.T} E={w.E} K={w.K} cuts={off.tolist()} cap={cap}")
+    want = B.qb_loop(batches, b0, w.K, off, threads=8)
+    zs = [torch.from_numpy(np.ascontiguousarray(z).view(np.int16)).cuda() for z in batches]
+    try:
+        eqb.eqb_set_max_blocks(cap)
+        got = eqb.qb_loop(zs, torch.from_numpy(b0), w.K, [int(x) for x in off])
+    finally:
+        eqb.eqb_set_max_blocks(0)
     check_loop(got, want)
 
 
